@@ -1,0 +1,435 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU needed).
+
+Each test states the property it checks and where it comes from.  They are chosen so that a
+plausible mistake in the oracle (a dropped term, a wrong sign or index, a transposed operand,
+a wrong tie rule) fails at least one of them.
+"""
+import fractions
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+from sklearn.metrics import mutual_info_score
+
+import oracle
+from paper_2106_05373_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def P(in_hcu=3, in_mcu=2, out_hcu=2, out_mcu=5, **kw):
+    return oracle.make_params(in_hcu, in_mcu, out_hcu, out_mcu, **kw)
+
+
+def rand_x(rng, B, in_hcu, in_mcu):
+    """Input rows whose activities sum to one within each input HCU."""
+    a = rng.random((B, in_hcu, in_mcu)) + 0.05
+    return (a / a.sum(-1, keepdims=True)).reshape(B, -1).astype(np.float32)
+
+
+def block_mask(mask, in_mcu, out_mcu):
+    return np.kron(mask, np.ones((in_mcu, out_mcu), np.uint8)).astype(bool)
+
+
+def trained_layer(p, steps=12, B=8, seed=0, mask=None):
+    rng = np.random.default_rng(seed)
+    L = oracle.OracleLayer(p, mask)
+    for _ in range(steps):
+        L.train_batch(rand_x(rng, B, p.in_hcu, p.in_mcu))
+    return L
+
+
+# ------------------------------------------------------------------------------------------
+# Counter-based generator and storage rounding
+# ------------------------------------------------------------------------------------------
+def test_splitmix_matches_published_sequence():
+    vals = [int(l, 16) for l in open(os.path.join(GOLDEN, "splitmix64_seed0.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(vals) == 3
+    for k, v in enumerate(vals):
+        assert oracle.splitmix_uniform(0, k) == (v >> 40) / 2.0 ** 24
+
+
+def test_bf16_rounding_matches_torch_rne():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(1)
+    v = np.concatenate([
+        rng.standard_normal(3000).astype(np.float32) * np.float32(10.0) ** rng.integers(-8, 8, 3000),
+        np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -(1.0 + 2.0 ** -8), 1.0 + 2.0 ** -8 + 2.0 ** -20,
+                  3.0e38, 3.4e38, 1e-40, 3e-39, -1e-45, 0.0, -0.0], np.float32),
+    ]).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float32).numpy()
+    got = np.array([oracle.round_storage(float(t), "bf16") for t in v], np.float32)
+    np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+    assert np.isinf(oracle.round_storage(float(np.float32(3.4e38)), "bf16"))
+    assert np.isnan(oracle.round_storage(float("nan"), "bf16"))
+
+
+def test_m10_rounding_matches_float16_in_its_normal_range():
+    # a 10-bit mantissa is IEEE half precision's; inside half's normal range the two agree.
+    rng = np.random.default_rng(2)
+    v = (rng.uniform(-1, 1, 4000) * 2.0 ** rng.uniform(-13, 15, 4000)).astype(np.float32)
+    v = np.concatenate([v, np.array([1 + 2.0 ** -11, 1 + 3 * 2.0 ** -11, 2.0 ** -14], np.float32)])
+    v = v[np.abs(v) >= 2.0 ** -14]
+    ref = v.astype(np.float16).astype(np.float32)
+    got = np.array([oracle.round_storage(float(t), "m10") for t in v], np.float32)
+    np.testing.assert_array_equal(got, ref)
+
+
+# ------------------------------------------------------------------------------------------
+# Initial state
+# ------------------------------------------------------------------------------------------
+def test_initial_state():
+    p = P(in_hcu=4, in_mcu=2, out_hcu=3, out_mcu=16, init_noise=0.25, seed=7)
+    mask = np.array([[1, 0, 1], [0, 1, 1], [1, 1, 0], [0, 0, 1]], np.uint8)
+    st = oracle.init_state(p, mask)
+    assert np.all(st["pi"] == np.float32(0.5)) and np.all(st["pj"] == np.float32(1 / 16))
+    assert np.all(st["pij"] == np.float32(0.5 / 16))
+    np.testing.assert_allclose(st["b"], np.log(1 / 16), rtol=1e-7)
+    bm = block_mask(mask, 2, 16)
+    assert np.all(st["w"][~bm] == 0)
+    assert np.all(np.abs(st["w"][bm]) <= 0.25)
+    n_out = 48
+    i, j = 3, 37
+    u = oracle.splitmix_uniform(7, i * n_out + j)
+    assert st["w"][i, j] == np.float32(0.25 * (2 * u - 1)) and bm[i, j]
+    # zero noise: the traces start independent, so every weight is log(1) = 0 and MI is 0.
+    p0 = P(in_hcu=4, in_mcu=2, out_hcu=3, out_mcu=16, init_noise=0.0)
+    st0 = oracle.init_state(p0, mask)
+    assert np.all(st0["w"] == 0)
+    w, _ = oracle.update_weights(p0, mask, st0["pi"], st0["pj"], st0["pij"])
+    assert np.all(w == 0)
+    assert np.all(oracle.mutual_information(p0, st0["pi"], st0["pj"], st0["pij"]) == 0)
+
+
+# ------------------------------------------------------------------------------------------
+# Support
+# ------------------------------------------------------------------------------------------
+def test_support_matches_fp64_matmul():
+    rng = np.random.default_rng(3)
+    p = P(in_hcu=7, in_mcu=3, out_hcu=4, out_mcu=6)
+    x = rng.random((9, 21)).astype(np.float32)
+    w = rng.standard_normal((21, 24)).astype(np.float32)
+    b = rng.standard_normal(24).astype(np.float32)
+    ref = (x.astype(np.float64) @ w.astype(np.float64) + b).astype(np.float32)
+    s = oracle.support(p, x, w, b)
+    np.testing.assert_allclose(s, ref, rtol=2e-7, atol=1e-6)
+
+
+def test_support_one_hot_row_gathers_one_weight_row():
+    rng = np.random.default_rng(4)
+    p = P(in_hcu=5, in_mcu=2, out_hcu=2, out_mcu=4)
+    w = rng.standard_normal((10, 8)).astype(np.float32)
+    b = rng.standard_normal(8).astype(np.float32)
+    x = np.eye(10, dtype=np.float32)
+    s = oracle.support(p, x, w, b)
+    np.testing.assert_array_equal(s, (w.astype(np.float64) + b).astype(np.float32))
+
+
+# ------------------------------------------------------------------------------------------
+# Softmax within each hidden HCU
+# ------------------------------------------------------------------------------------------
+def test_softmax_matches_scipy_and_sums_to_one():
+    rng = np.random.default_rng(5)
+    p = P(out_hcu=3, out_mcu=7, gain=1.7)
+    s = (rng.standard_normal((11, 21)) * 5).astype(np.float32)
+    y = oracle.softmax(p, s)
+    ref = scipy.special.softmax(1.7 * s.astype(np.float64).reshape(11, 3, 7), axis=-1)
+    np.testing.assert_allclose(y, ref.reshape(11, 21), rtol=3e-7, atol=1e-12)
+    np.testing.assert_allclose(y.reshape(11, 3, 7).sum(-1, dtype=np.float64), 1.0, atol=1e-6)
+
+
+def test_softmax_special_cases():
+    rng = np.random.default_rng(6)
+    s = (rng.standard_normal((4, 12)) * 3).astype(np.float32)
+    # shifting one HCU's support by a constant changes nothing (up to rounding)
+    p = P(out_hcu=2, out_mcu=6)
+    s2 = s.copy()
+    s2[:, :6] += np.float32(3.0)
+    np.testing.assert_allclose(oracle.softmax(p, s2), oracle.softmax(p, s), atol=2e-6)
+    # gain 0 -> exactly uniform
+    assert np.all(oracle.softmax(P(out_hcu=2, out_mcu=6, gain=0.0), s) == np.float32(1 / 6))
+    # one MCU per HCU -> exactly 1
+    assert np.all(oracle.softmax(P(out_hcu=12, out_mcu=1), s) == 1.0)
+    # two MCUs -> the logistic function of the gained difference
+    y = oracle.softmax(P(out_hcu=6, out_mcu=2, gain=0.6), s)
+    d = 0.6 * (s[:, 0::2].astype(np.float64) - s[:, 1::2])
+    np.testing.assert_allclose(y[:, 0::2], scipy.special.expit(d), rtol=1e-6, atol=1e-30)
+
+
+# ------------------------------------------------------------------------------------------
+# Trace updates (exponential moving averages)
+# ------------------------------------------------------------------------------------------
+def test_traces_closed_form_under_constant_input():
+    # gain 0 makes y constant (1 / M_out); with a constant input row every trace follows
+    # P_k = t + (1 - a)^k (P_0 - t) with t the batch average.
+    rng = np.random.default_rng(7)
+    a, k = 0.05, 40
+    p = P(in_hcu=3, in_mcu=2, out_hcu=2, out_mcu=4, alpha=a, gain=0.0)
+    L = oracle.OracleLayer(p)
+    row = rand_x(rng, 1, 3, 2)
+    x = np.repeat(row, 5, axis=0)
+    pi0, pj0, pij0 = L.pi.astype(np.float64), L.pj.astype(np.float64), L.pij.astype(np.float64)
+    for _ in range(k):
+        L.train_batch(x)
+    d = (1 - a) ** k
+    ti = row[0].astype(np.float64)
+    tij = np.outer(ti, np.full(8, 0.25))
+    np.testing.assert_allclose(L.pi, ti + d * (pi0 - ti), atol=k * 6e-8)
+    np.testing.assert_allclose(L.pj, 0.25 + d * (pj0 - 0.25), atol=k * 6e-8)
+    np.testing.assert_allclose(L.pij, tij + d * (pij0 - tij), atol=k * 6e-8)
+
+
+def test_n_cycles_equals_one_cycle_with_effective_rate():
+    rng = np.random.default_rng(8)
+    a, n = 0.02, 3
+    p3 = P(alpha=a, n_cycles=n)
+    p1 = P(alpha=1 - (1 - a) ** n, n_cycles=1)
+    L = trained_layer(p1, steps=3)
+    x = rand_x(rng, 6, 3, 2)
+    y = rng.random((6, 10)).astype(np.float32)
+    r3 = oracle.update_traces(p3, x, y, L.pi, L.pj, L.pij)
+    r1 = oracle.update_traces(p1, x, y, L.pi, L.pj, L.pij)
+    for u, v in zip(r3, r1):
+        np.testing.assert_allclose(u, v, rtol=3e-7, atol=1e-9)
+
+
+def test_traces_match_per_sample_outer_products():
+    # <a_i (x) a_j> written as a loop of explicit per-sample outer products.
+    rng = np.random.default_rng(9)
+    a = 0.1
+    p = P(in_hcu=4, in_mcu=3, out_hcu=3, out_mcu=5, alpha=a)
+    L = trained_layer(p, steps=2)
+    x = rand_x(rng, 7, 4, 3)
+    y = rng.random((7, 15)).astype(np.float32)
+    pi, pj, pij = oracle.update_traces(p, x, y, L.pi, L.pj, L.pij)
+    acc = np.zeros((12, 15))
+    for r in range(7):
+        acc += np.outer(x[r].astype(np.float64), y[r].astype(np.float64))
+    np.testing.assert_allclose(pij, (1 - a) * L.pij + a * acc / 7, rtol=3e-7, atol=1e-12)
+    np.testing.assert_allclose(pi, (1 - a) * L.pi + a * x.astype(np.float64).mean(0), rtol=3e-7)
+    np.testing.assert_allclose(pj, (1 - a) * L.pj + a * y.astype(np.float64).mean(0), rtol=3e-7)
+
+
+def test_trace_invariants_hold_at_every_step():
+    # With HCU-normalised activities on both sides, every HCU's Pi and Pj sum to one and the
+    # joint trace's block sums reproduce the marginals (exact in real arithmetic).
+    w = synth.WORKLOADS["tiny"]
+    px, _ = synth.dataset(w, n=256)
+    X = synth.encode_pixels(px)
+    p = oracle.make_params(64, 2, 4, 16, alpha=0.05, seed=0)
+    L = oracle.OracleLayer(p)
+    for k in range(8):
+        L.train_batch(X[32 * k:32 * (k + 1)])
+        np.testing.assert_allclose(L.pi.reshape(64, 2).sum(-1, dtype=np.float64), 1, atol=2e-6)
+        np.testing.assert_allclose(L.pj.reshape(4, 16).sum(-1, dtype=np.float64), 1, atol=2e-6)
+        blocks = L.pij.astype(np.float64).reshape(64, 2, 4, 16)
+        np.testing.assert_allclose(blocks.sum(-1).reshape(128, 4),
+                                   np.repeat(L.pi[:, None], 4, 1), atol=2e-7)
+        np.testing.assert_allclose(blocks.sum(1).reshape(64, 64),
+                                   np.repeat(L.pj[None, :], 64, 0), atol=2e-7)
+
+
+# ------------------------------------------------------------------------------------------
+# Weights, bias and mask
+# ------------------------------------------------------------------------------------------
+def test_weights_vanish_for_independent_activity():
+    # gain 0: the hidden activity does not depend on the input, so Pij stays Pi (x) Pj and
+    # every weight log(Pij / (Pi Pj)) stays 0 up to rounding; the bias is log(1 / M_out).
+    rng = np.random.default_rng(10)
+    p = P(in_hcu=5, in_mcu=2, out_hcu=3, out_mcu=8, alpha=0.1, gain=0.0, init_noise=0.3)
+    L = oracle.OracleLayer(p)
+    for _ in range(15):
+        L.train_batch(rand_x(rng, 9, 5, 2))
+        assert np.abs(L.w).max() < 2e-6
+        np.testing.assert_allclose(L.b, np.log(1 / 8), rtol=1e-6)
+
+
+def test_weights_log_ratio_and_mask():
+    p = P(in_hcu=3, in_mcu=2, out_hcu=2, out_mcu=5, eps=1e-3, bias_gain=0.7)
+    rng = np.random.default_rng(11)
+    pi = rng.random(6).astype(np.float32)
+    pj = rng.random(10).astype(np.float32)
+    pij = rng.random((6, 10)).astype(np.float32)
+    pij[0, 0] = 0.0                     # clamped to eps inside the log
+    pj[3] = 1e-5
+    mask = np.array([[1, 0], [0, 1], [1, 1]], np.uint8)
+    w, b = oracle.update_weights(p, mask, pi, pj, pij)
+    c = lambda v: np.maximum(v.astype(np.float64), np.float64(np.float32(1e-3)))
+    ref = np.log(c(pij) / np.outer(c(pi), c(pj)))
+    bm = block_mask(mask, 2, 5)
+    np.testing.assert_allclose(w[bm], ref[bm], rtol=1e-6, atol=1e-7)
+    assert np.all(w[~bm] == 0)
+    np.testing.assert_allclose(b, 0.7 * np.log(c(pj)), rtol=1e-6)
+
+
+# ------------------------------------------------------------------------------------------
+# Mutual information
+# ------------------------------------------------------------------------------------------
+def test_mutual_information_matches_textbook_on_single_blocks():
+    # sklearn's mutual_info_score takes a contingency table of counts; the joint trace of one
+    # (input HCU, hidden HCU) pair is that table normalised, with its row and column sums as
+    # the marginals.
+    rng = np.random.default_rng(12)
+    for m_in, m_out in [(2, 2), (2, 7), (3, 5), (4, 16)]:
+        counts = rng.integers(0, 40, (m_in, m_out))
+        counts[0, -1] = 0
+        joint = (counts / counts.sum()).astype(np.float32)
+        pi = (counts.sum(1) / counts.sum()).astype(np.float32)
+        pj = (counts.sum(0) / counts.sum()).astype(np.float32)
+        p = P(in_hcu=1, in_mcu=m_in, out_hcu=1, out_mcu=m_out, eps=1e-30)
+        mi = oracle.mutual_information(p, pi, pj, joint)
+        ref = mutual_info_score(None, None, contingency=counts)
+        np.testing.assert_allclose(mi[0, 0], ref, rtol=1e-6, atol=1e-9)
+
+
+def test_mutual_information_extremes():
+    p = P(in_hcu=1, in_mcu=2, out_hcu=1, out_mcu=2)
+    half = np.float32(0.5)
+    diag = np.array([[0.5, 0.0], [0.0, 0.5]], np.float32)
+    mi = oracle.mutual_information(p, np.array([half, half]), np.array([half, half]), diag)
+    assert mi[0, 0] == pytest.approx(np.log(2), rel=1e-12)
+    indep = np.full((2, 2), 0.25, np.float32)
+    assert oracle.mutual_information(p, np.array([half, half]), np.array([half, half]),
+                                     indep)[0, 0] == 0.0
+
+
+def test_mutual_information_per_block_on_a_trained_layer():
+    p = P(in_hcu=5, in_mcu=2, out_hcu=3, out_mcu=6, alpha=0.2, gain=3.0, eps=1e-30)
+    L = trained_layer(p, steps=25, B=16, seed=13)
+    mi = oracle.mutual_information(p, L.pi, L.pj, L.pij)
+    assert mi.shape == (5, 3)
+    for hi in range(5):
+        for hj in range(3):
+            # MI = H(rows) + H(columns) - H(joint) of the block (entropy identity)
+            blk = L.pij[2 * hi:2 * hi + 2, 6 * hj:6 * hj + 6].astype(np.float64)
+            ref = (scipy.stats.entropy(blk.sum(1)) + scipy.stats.entropy(blk.sum(0))
+                   - scipy.stats.entropy(blk.ravel()))
+            np.testing.assert_allclose(mi[hi, hj], ref, rtol=1e-4, atol=1e-6)
+    assert np.all(mi >= -1e-7) and np.all(mi <= np.log(2) + 1e-6)
+
+
+# ------------------------------------------------------------------------------------------
+# Greedy swap
+# ------------------------------------------------------------------------------------------
+def _brute_swap(mi, mask, n_swaps):
+    """All (active, silent) pairs of each hidden HCU, best exact gain first, ties to the
+    lowest active then lowest silent index; repeated over HCUs not yet swapped."""
+    mask = mask.copy()
+    for hj in range(mask.shape[1]):
+        used = set()
+        for _ in range(n_swaps):
+            best = None
+            for a in range(mask.shape[0]):
+                if not mask[a, hj] or a in used:
+                    continue
+                for s in range(mask.shape[0]):
+                    if mask[s, hj] or s in used:
+                        continue
+                    gain = fractions.Fraction(mi[s, hj]) - fractions.Fraction(mi[a, hj])
+                    key = (gain, -a, -s)
+                    if best is None or key > best[0]:
+                        best = (key, a, s)
+            if best is None or best[0][0] <= 0:
+                break
+            _, a, s = best
+            mask[a, hj], mask[s, hj] = 0, 1
+            used |= {a, s}
+    return mask
+
+
+@pytest.mark.parametrize("n_swaps", [1, 2, 3])
+def test_swap_matches_brute_force(n_swaps):
+    rng = np.random.default_rng(20 + n_swaps)
+    for trial in range(30):
+        hin, hout, k = 9, 4, 4
+        mask = np.stack([synth.random_mask(hin, 1, k, 100 * trial + c)[:, 0] for c in range(hout)], 1)
+        mi = rng.integers(0, 6, (hin, hout)).astype(np.float64) * 0.125   # many exact ties
+        if trial % 3 == 0:
+            mi = rng.random((hin, hout))
+        p = P(in_hcu=hin, out_hcu=hout, n_swaps=n_swaps)
+        n, new, swaps = oracle.plasticity_swap(p, mi, mask)
+        np.testing.assert_array_equal(new, _brute_swap(mi, mask, n_swaps))
+        np.testing.assert_array_equal(new.sum(0), mask.sum(0))
+        assert n == int((new != mask).sum() // 2)
+
+
+def test_swap_requires_strict_gain():
+    p = P(in_hcu=4, out_hcu=1)
+    mask = np.array([[1], [1], [0], [0]], np.uint8)
+    mi = np.array([[0.3], [0.2], [0.2], [0.1]])
+    n, new, _ = oracle.plasticity_swap(p, mi, mask)
+    assert n == 0 and np.array_equal(new, mask)
+    mi[3, 0] = np.nextafter(0.2, 1)
+    n, new, swaps = oracle.plasticity_swap(p, mi, mask)
+    assert n == 1 and list(swaps[0, 0]) == [1, 3]
+    assert list(new[:, 0]) == [1, 0, 0, 1]
+
+
+def test_structural_update_patches_swapped_blocks():
+    p = P(in_hcu=6, in_mcu=2, out_hcu=3, out_mcu=4, alpha=0.3, gain=2.0)
+    mask = np.stack([synth.random_mask(6, 1, 2, c)[:, 0] for c in range(3)], 1)
+    L = trained_layer(p, steps=10, mask=mask)
+    n, mi, swaps = L.structural_update()
+    assert n > 0
+    w_ref, _ = oracle.update_weights(p, L.mask, L.pi, L.pj, L.pij)
+    np.testing.assert_array_equal(L.w, w_ref)
+    assert np.array_equal(L.mask.sum(0), mask.sum(0))
+
+
+# ------------------------------------------------------------------------------------------
+# Readout and the whole step
+# ------------------------------------------------------------------------------------------
+def test_readout_argmax_lowest_index_on_ties():
+    rng = np.random.default_rng(30)
+    s = rng.integers(0, 4, (50, 12)).astype(np.float32)      # many ties
+    p = P(out_hcu=3, out_mcu=4)
+    win = oracle.readout(p, s)
+    np.testing.assert_array_equal(win, s.reshape(50, 3, 4).argmax(-1))
+
+
+def test_train_batch_matches_per_sample_formulation():
+    rng = np.random.default_rng(31)
+    a = 0.07
+    p = P(in_hcu=5, in_mcu=2, out_hcu=3, out_mcu=4, alpha=a, gain=1.3, eps=1e-6)
+    mask = np.array([[1, 0, 1], [1, 1, 0], [0, 1, 1], [1, 1, 1], [0, 0, 1]], np.uint8)
+    L = trained_layer(p, steps=4, mask=mask)
+    before = L.get_state()
+    x = rand_x(rng, 6, 5, 2)
+    s, y = L.train_batch(x)
+    xd = x.astype(np.float64)
+    pi, pj, pij = (before[k].astype(np.float64) for k in ("pi", "pj", "pij"))
+    w, b = before["w"].astype(np.float64), before["b"].astype(np.float64)
+    s_ref = np.stack([b + xd[r] @ w for r in range(6)])
+    y_ref = scipy.special.softmax(1.3 * s_ref.reshape(6, 3, 4), axis=-1).reshape(6, 12)
+    outer = sum(np.outer(xd[r], y_ref[r]) for r in range(6)) / 6
+    pi_n = (1 - a) * pi + a * xd.mean(0)
+    pj_n = (1 - a) * pj + a * y_ref.mean(0)
+    pij_n = (1 - a) * pij + a * outer
+    e = np.float64(np.float32(1e-6))
+    w_n = np.log(np.maximum(pij_n, e) / np.outer(np.maximum(pi_n, e), np.maximum(pj_n, e)))
+    w_n[~block_mask(mask, 2, 4)] = 0
+    np.testing.assert_allclose(s, s_ref, rtol=1e-6, atol=1e-6)
+    np.testing.assert_allclose(y, y_ref, rtol=1e-5, atol=1e-7)
+    np.testing.assert_allclose(L.pi, pi_n, rtol=3e-7)
+    np.testing.assert_allclose(L.pj, pj_n, rtol=1e-6)
+    np.testing.assert_allclose(L.pij, pij_n, rtol=1e-6)
+    np.testing.assert_allclose(L.w, w_n, atol=3e-6)
+    np.testing.assert_allclose(L.b, np.log(np.maximum(pj_n, e)), rtol=1e-6)
+
+
+def test_supervised_target_replaces_activity():
+    rng = np.random.default_rng(32)
+    p = P(in_hcu=4, in_mcu=2, out_hcu=1, out_mcu=3, alpha=0.2)
+    L1 = trained_layer(p, steps=2)
+    L2 = oracle.OracleLayer(p)
+    L2.set_state(L1.get_state())
+    x = rand_x(rng, 5, 4, 2)
+    t = synth.one_hot(np.array([0, 2, 1, 2, 2]), 3)
+    L1.train_batch(x, target=t)
+    pi, pj, pij = oracle.update_traces(p, x, t, L2.pi, L2.pj, L2.pij)
+    np.testing.assert_array_equal(L1.pij, pij)
+    np.testing.assert_array_equal(L1.pj, pj)
+    np.testing.assert_allclose(L1.pj, 0.8 * L2.pj + 0.2 * t.mean(0), rtol=1e-6)
