@@ -1,0 +1,158 @@
+/*
+ * bcpnn.h -- C ABI of the BCPNN hidden-layer training library for AMD MI355X (gfx950).
+ *
+ * The library implements one layer of the Bayesian Confidence Propagation Neural Network as
+ * trained by StreamBrain (Podobas et al., HEART 2021, Sec. 2, Algorithm 1):
+ *
+ *   support      s_j  = b_j + sum_i a_i w_ij          (w already masked)      Alg. 1, support line
+ *   activation   a_j  = softmax over the hidden HCU of g * s_j                 Alg. 1; Sec. 2
+ *   traces       C_i  <- (1-l) C_i  + l <a_i>                                 Alg. 1, cycle loop
+ *                C_j  <- (1-l) C_j  + l <a_j>
+ *                C_ij <- (1-l) C_ij + l <a_i a_j>   (<.> = mean over the batch)
+ *   weights      w_ij = log(C_ij / (C_i C_j)),  b_j = k_B log C_j,  w *= mask   Alg. 1
+ *   plasticity   per hidden HCU, swap the active input HCU of lowest mutual
+ *                information for the silent one of highest                  Sec. 2, last paragraph
+ *
+ * Terms: an HCU (hypercolumn) is a group of MCUs (minicolumns) whose activities form one
+ * discrete distribution.  Units are numbered HCU-major: unit = hcu * M + mcu.  C_i, C_j, C_ij
+ * are called Pi, Pj, Pij below and l is `alpha`.
+ *
+ * Layouts (row-major, fp32 unless stated):
+ *   x       [B][N_in]            input activities, N_in = in_hcu * in_mcu
+ *   y, s    [B][N_out]           hidden activities / support, N_out = out_hcu * out_mcu
+ *   target  [B][N_out]           clamped activities for supervised training
+ *   winner  [B][out_hcu] int32   argmax MCU index of each hidden HCU
+ *   pi [N_in], pj [N_out], b [N_out]
+ *   pij, w  [N_in][N_out]        i-major: block (hi, hj) is in_mcu rows x out_mcu columns
+ *   mask    [in_hcu][out_hcu] uint8, 1 = active connection, 0 = silent
+ *
+ * Ownership and streams: the layer owns every state buffer (allocated in create, freed in
+ * destroy).  Caller buffers named *_dev are device pointers (16-byte aligned, contiguous) that
+ * the caller owns; *_host are host pointers.  Every call enqueues its kernels on the stream
+ * given to create and returns without waiting, except get_state, set_state, get_mi and
+ * structural_update with a non-NULL count pointer, which wait for the stream.  Calls on one
+ * layer must not run concurrently from several host threads.
+ *
+ * Errors: every call returns a bcpnn_status.  Arguments are checked on the host before any
+ * device work; BCPNN_EINVAL leaves the layer unchanged.  A failed HIP call returns
+ * BCPNN_EDEVICE and marks the layer failed: later calls on it return BCPNN_ESTATE (destroy
+ * still works).  bcpnn_last_error() describes the last failure of the calling thread.
+ */
+#ifndef BCPNN_H
+#define BCPNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct bcpnn_layer bcpnn_layer;
+
+typedef enum {
+    BCPNN_OK = 0,
+    BCPNN_EINVAL = -1,   /* invalid argument; nothing was changed                        */
+    BCPNN_ENOMEM = -2,   /* device or host allocation failed                             */
+    BCPNN_EDEVICE = -3,  /* a HIP call failed; the layer is now unusable                 */
+    BCPNN_ESTATE = -4    /* the layer failed earlier                                     */
+} bcpnn_status;
+
+/* Storage format of Pij and W.  F32 stores fp32.  BF16 and M10 keep fp32 arrays whose values
+ * are rounded to nearest-even to 7 (bfloat16) or 10 mantissa bits after every update; the
+ * paper's FPGA backend varies this width (Sec. 3, FPGA backend).  Arithmetic stays fp32. */
+typedef enum { BCPNN_STORE_F32 = 0, BCPNN_STORE_BF16 = 1, BCPNN_STORE_M10 = 2 } bcpnn_storage;
+
+typedef struct {
+    int32_t in_hcu, in_mcu;     /* input HCUs and MCUs per HCU (> 0)                          */
+    int32_t out_hcu, out_mcu;   /* hidden HCUs and MCUs per HCU (> 0, out_mcu <= 1024)         */
+    int32_t max_batch;          /* largest B accepted by forward/train_batch/readout (> 0)    */
+    float alpha;                /* trace rate l of Alg. 1, in (0, 1]; from a time constant
+                                   tau (in batches) use alpha = 1 / tau                      */
+    int32_t n_cycles;           /* repetitions of the trace/weight cycle per batch (>= 1);
+                                   equivalent to one cycle at 1 - (1 - alpha)^n_cycles        */
+    float gain;                 /* softmax gain g (>= 0, finite); 1 is the paper's softmax    */
+    float bias_gain;            /* k_B of Alg. 1 (finite)                                     */
+    float eps;                  /* lower clamp of each probability inside a log (> 0)         */
+    float pi_init, pj_init;     /* initial Pi, Pj; <= 0 selects 1 / in_mcu, 1 / out_mcu        */
+    float init_noise;           /* initial w = mask * init_noise * (2u - 1), u ~ U[0, 1) from
+                                   the SplitMix64 finaliser of (seed, i * N_out + j)          */
+    uint64_t seed;
+    int32_t n_swaps;            /* swaps per hidden HCU per structural update (>= 0)          */
+    int32_t storage;            /* bcpnn_storage                                              */
+} bcpnn_config;
+
+/* Host-side view of the layer state (fp32 arrays and the uint8 mask, layouts above). */
+typedef struct {
+    float *pi, *pj, *pij, *w, *b;
+    uint8_t *mask;
+} bcpnn_state_view;
+
+/* Fills cfg with the defaults (alpha 1e-3, one cycle, gain 1, k_B 1, eps 1e-8, uniform initial
+ * traces, init_noise 0.1, seed 0, one swap, fp32 storage) for the given sizes. */
+void bcpnn_config_default(bcpnn_config *cfg, int32_t in_hcu, int32_t in_mcu, int32_t out_hcu,
+                          int32_t out_mcu, int32_t max_batch);
+
+/* Creates a layer (Alg. 1 initial state): Pi = pi_init, Pj = pj_init, Pij = Pi * Pj,
+ * b = k_B log Pj, w = the masked noise described at init_noise.  mask_host is
+ * [in_hcu][out_hcu] of 0/1 (NULL = every connection active); every hidden HCU needs at least
+ * one active input HCU.  hip_stream is a hipStream_t (NULL = the null stream).  The layer
+ * allocates about 8 * N_in * N_out bytes of device memory plus batch buffers.
+ * Errors: EINVAL (sizes, rates, mask), ENOMEM, EDEVICE. */
+bcpnn_status bcpnn_layer_create(const bcpnn_config *cfg, const uint8_t *mask_host,
+                                void *hip_stream, bcpnn_layer **out);
+
+/* Releases the layer and its device memory after its stream is idle.  NULL is ignored. */
+void bcpnn_layer_destroy(bcpnn_layer *layer);
+
+/* Inference (Alg. 1 support and softmax lines, no learning): y_dev [B][N_out] receives the
+ * activities; s_dev (nullable) the support.  1 <= B <= max_batch. */
+bcpnn_status bcpnn_forward(bcpnn_layer *layer, const float *x_dev, int32_t B, float *y_dev,
+                           float *s_dev);
+
+/* One training batch, Alg. 1 from the batch input to "apply mask" (support, softmax, the
+ * n_cycles trace updates with the batch means, weights, bias, mask).  If target_dev is not NULL
+ * its rows replace the softmax activity in the trace updates (supervised output layer, Sec. 2).
+ * y_dev (nullable) receives the softmax activities.  1 <= B <= max_batch; the means divide by B. */
+bcpnn_status bcpnn_train_batch(bcpnn_layer *layer, const float *x_dev, int32_t B,
+                               const float *target_dev, float *y_dev);
+
+/* Recomputes w and b from the current traces and mask (Alg. 1 weight, bias and mask lines). */
+bcpnn_status bcpnn_recompute_weights(bcpnn_layer *layer);
+
+/* Structural plasticity (Alg. 1 "update plasticity mask"; Sec. 2): scores every
+ * (input HCU, hidden HCU) pair by the mutual information of its block of Pij (fp64), then for
+ * each hidden HCU swaps, up to n_swaps times, the active input HCU of lowest score for the
+ * silent one of highest score when that score is strictly larger (ties: lowest HCU index), and
+ * rewrites the changed blocks of w.  The caller schedules it (before a batch).
+ * n_swapped_host (nullable) receives the number of swaps; passing it waits for the stream. */
+bcpnn_status bcpnn_structural_update(bcpnn_layer *layer, int32_t *n_swapped_host);
+
+/* Readout: winner_dev [B][out_hcu] receives, for each sample and hidden HCU, the MCU index of
+ * the largest support (ties: lowest index). */
+bcpnn_status bcpnn_readout(bcpnn_layer *layer, const float *x_dev, int32_t B,
+                           int32_t *winner_dev);
+
+/* Copies the state to host arrays (each pointer of the view may be NULL to skip it).  Waits. */
+bcpnn_status bcpnn_get_state(const bcpnn_layer *layer, const bcpnn_state_view *host_out);
+
+/* Replaces the state from host arrays (all six pointers required).  The mask must satisfy the
+ * create rules; w is stored with the mask applied (silent blocks become 0).  Waits. */
+bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in);
+
+/* Copies the mutual-information scores of the last structural update, [in_hcu][out_hcu] fp64,
+ * to the host.  Waits.  EINVAL before the first structural update. */
+bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
+
+/* Kernel timing for measurement: while enabled, the library records HIP events on its stream
+ * around every launch of the joint-trace kernel.  bcpnn_profile_read waits for the stream and
+ * returns the summed duration (ms) and count of the launches since the last read. */
+bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t enable);
+bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
+
+/* Message of the calling thread's last failure ("" if none). */
+const char *bcpnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BCPNN_H */

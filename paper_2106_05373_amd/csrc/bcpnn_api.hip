@@ -1,0 +1,425 @@
+// C ABI of libbcpnn (declared in include/bcpnn.h): argument checks, state ownership, launches.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "bcpnn_internal.h"
+
+using bcpnn::Geometry;
+
+namespace {
+
+constexpr int32_t kMaxOutMcu = 1024;     // softmax segment held in LDS by the support kernel
+constexpr int32_t kMaxInHcu = 49152;     // mask column held in LDS by the swap kernel
+constexpr int32_t kMaxSwaps = 256;
+
+thread_local std::string g_error;
+
+bcpnn_status fail(bcpnn_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+}  // namespace
+
+struct bcpnn_layer {
+    bcpnn_config cfg;
+    Geometry g;
+    hipStream_t stream = nullptr;
+    int drop_bits = 0;
+    float* pi[2] = {nullptr, nullptr};   // the trace kernel reads one and writes the other
+    float* pj[2] = {nullptr, nullptr};
+    int cur = 0;
+    float* pij = nullptr;
+    float* w = nullptr;
+    float* b = nullptr;
+    uint8_t* mask = nullptr;             // [in_hcu][out_hcu]
+    int32_t* act_list = nullptr;         // [out_hcu][in_hcu], ascending active input HCUs
+    int32_t* act_count = nullptr;        // [out_hcu]
+    int32_t* swap_count = nullptr;       // [out_hcu]
+    double* mi = nullptr;                // [in_hcu][out_hcu]
+    float* y_buf = nullptr;              // [max_batch][n_out] activity when the caller gives none
+    bool mi_valid = false;
+    bool failed = false;
+    bool profiling = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+    size_t events_used = 0;
+};
+
+#define HIP_TRY(layer, expr)                                                             \
+    do {                                                                                 \
+        hipError_t e_ = (expr);                                                          \
+        if (e_ != hipSuccess) {                                                          \
+            (layer)->failed = true;                                                      \
+            return fail(BCPNN_EDEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));  \
+        }                                                                                \
+    } while (0)
+
+namespace {
+
+const char* check_config(const bcpnn_config* c) {
+    if (!c) return "config is NULL";
+    if (c->in_hcu <= 0 || c->in_mcu <= 0 || c->out_hcu <= 0 || c->out_mcu <= 0)
+        return "HCU and MCU counts must be positive";
+    if (c->out_mcu > kMaxOutMcu) return "out_mcu exceeds 1024";
+    if (c->in_hcu > kMaxInHcu) return "in_hcu exceeds 49152";
+    const int64_t n_in = (int64_t)c->in_hcu * c->in_mcu, n_out = (int64_t)c->out_hcu * c->out_mcu;
+    if (n_in > (1ll << 31) - 1 || n_out > (1ll << 31) - 1) return "unit counts exceed 2^31 - 1";
+    if ((n_in + 127) / 128 > 65535) return "N_in exceeds 65535 * 128";
+    if (c->max_batch <= 0) return "max_batch must be positive";
+    if (!(c->alpha > 0.0f && c->alpha <= 1.0f)) return "alpha must lie in (0, 1]";
+    if (c->n_cycles < 1) return "n_cycles must be >= 1";
+    if (!(c->gain >= 0.0f) || !isfinite(c->gain)) return "gain must be finite and >= 0";
+    if (!isfinite(c->bias_gain)) return "bias_gain must be finite";
+    if (!(c->eps > 0.0f) || !isfinite(c->eps)) return "eps must be finite and > 0";
+    if (!isfinite(c->pi_init) || !isfinite(c->pj_init) || c->pi_init > 1.0f || c->pj_init > 1.0f)
+        return "pi_init / pj_init must be finite and <= 1";
+    if (!isfinite(c->init_noise) || c->init_noise < 0.0f) return "init_noise must be finite and >= 0";
+    if (c->n_swaps < 0 || c->n_swaps > kMaxSwaps) return "n_swaps must lie in [0, 256]";
+    if (c->storage != BCPNN_STORE_F32 && c->storage != BCPNN_STORE_BF16 &&
+        c->storage != BCPNN_STORE_M10)
+        return "unknown storage format";
+    return nullptr;
+}
+
+// Checks a host mask and builds the per-hidden-HCU active lists.
+const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
+                               std::vector<int32_t>& list, std::vector<int32_t>& count) {
+    list.assign((size_t)c.out_hcu * c.in_hcu, 0);
+    count.assign((size_t)c.out_hcu, 0);
+    for (int32_t hi = 0; hi < c.in_hcu; ++hi)
+        for (int32_t hj = 0; hj < c.out_hcu; ++hj) {
+            const uint8_t m = mask ? mask[(size_t)hi * c.out_hcu + hj] : 1;
+            if (m > 1) return "mask entries must be 0 or 1";
+            if (m) list[(size_t)hj * c.in_hcu + count[hj]++] = hi;
+        }
+    for (int32_t hj = 0; hj < c.out_hcu; ++hj)
+        if (count[hj] == 0) return "every hidden HCU needs at least one active input HCU";
+    return nullptr;
+}
+
+void free_layer(bcpnn_layer* L) {
+    if (!L) return;
+    void* bufs[] = {L->pi[0], L->pi[1], L->pj[0], L->pj[1], L->pij, L->w, L->b, L->mask,
+                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf};
+    for (void* p : bufs)
+        if (p) (void)hipFree(p);
+    for (auto& ev : L->events) {
+        (void)hipEventDestroy(ev.first);
+        (void)hipEventDestroy(ev.second);
+    }
+    delete L;
+}
+
+bcpnn_status usable(const bcpnn_layer* L) {
+    if (!L) return fail(BCPNN_EINVAL, "layer is NULL");
+    if (L->failed) return fail(BCPNN_ESTATE, "layer failed earlier: %s", g_error.c_str());
+    return BCPNN_OK;
+}
+
+bcpnn_status check_batch(const bcpnn_layer* L, int32_t B) {
+    if (B < 1 || B > L->cfg.max_batch)
+        return fail(BCPNN_EINVAL, "batch %d outside [1, %d]", B, L->cfg.max_batch);
+    return BCPNN_OK;
+}
+
+template <typename T>
+hipError_t dalloc(T** p, size_t n) {
+    return hipMalloc((void**)p, n * sizeof(T) ? n * sizeof(T) : 1);
+}
+
+}  // namespace
+
+extern "C" {
+
+void bcpnn_config_default(bcpnn_config* c, int32_t in_hcu, int32_t in_mcu, int32_t out_hcu,
+                          int32_t out_mcu, int32_t max_batch) {
+    if (!c) return;
+    memset(c, 0, sizeof *c);
+    c->in_hcu = in_hcu;
+    c->in_mcu = in_mcu;
+    c->out_hcu = out_hcu;
+    c->out_mcu = out_mcu;
+    c->max_batch = max_batch;
+    c->alpha = 1e-3f;
+    c->n_cycles = 1;
+    c->gain = 1.0f;
+    c->bias_gain = 1.0f;
+    c->eps = 1e-8f;
+    c->pi_init = 0.0f;
+    c->pj_init = 0.0f;
+    c->init_noise = 0.1f;
+    c->seed = 0;
+    c->n_swaps = 1;
+    c->storage = BCPNN_STORE_F32;
+}
+
+const char* bcpnn_last_error(void) { return g_error.c_str(); }
+
+bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_host,
+                                void* hip_stream, bcpnn_layer** out) {
+    if (!out) return fail(BCPNN_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (const char* why = check_config(cfg)) return fail(BCPNN_EINVAL, "%s", why);
+    std::vector<int32_t> list, count;
+    if (const char* why = build_active_lists(*cfg, mask_host, list, count))
+        return fail(BCPNN_EINVAL, "%s", why);
+
+    bcpnn_layer* L = new bcpnn_layer();
+    L->cfg = *cfg;
+    L->g = Geometry{cfg->in_hcu, cfg->in_mcu, cfg->out_hcu, cfg->out_mcu,
+                    (int64_t)cfg->in_hcu * cfg->in_mcu, (int64_t)cfg->out_hcu * cfg->out_mcu};
+    L->stream = (hipStream_t)hip_stream;
+    L->drop_bits = bcpnn::storage_drop_bits(cfg->storage);
+    const Geometry& g = L->g;
+    const size_t E = (size_t)g.n_in * (size_t)g.n_out;
+    const size_t hh = (size_t)cfg->in_hcu * cfg->out_hcu;
+
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < 2 && e == hipSuccess; ++k) {
+        e = dalloc(&L->pi[k], (size_t)g.n_in);
+        if (e == hipSuccess) e = dalloc(&L->pj[k], (size_t)g.n_out);
+    }
+    if (e == hipSuccess) e = dalloc(&L->pij, E);
+    if (e == hipSuccess) e = dalloc(&L->w, E);
+    if (e == hipSuccess) e = dalloc(&L->b, (size_t)g.n_out);
+    if (e == hipSuccess) e = dalloc(&L->mask, hh);
+    if (e == hipSuccess) e = dalloc(&L->act_list, hh);
+    if (e == hipSuccess) e = dalloc(&L->act_count, (size_t)cfg->out_hcu);
+    if (e == hipSuccess) e = dalloc(&L->swap_count, (size_t)cfg->out_hcu);
+    if (e == hipSuccess) e = dalloc(&L->mi, hh);
+    if (e == hipSuccess) e = dalloc(&L->y_buf, (size_t)cfg->max_batch * g.n_out);
+    if (e != hipSuccess) {
+        free_layer(L);
+        return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,
+                    "device allocation failed: %s", hipGetErrorString(e));
+    }
+
+    std::vector<uint8_t> mask(hh, 1);
+    if (mask_host) memcpy(mask.data(), mask_host, hh);
+    const double pi0d = cfg->pi_init > 0.0f ? (double)cfg->pi_init : 1.0 / cfg->in_mcu;
+    const double pj0d = cfg->pj_init > 0.0f ? (double)cfg->pj_init : 1.0 / cfg->out_mcu;
+    const float pi0 = (float)pi0d, pj0 = (float)pj0d;
+    const float pij0 = (float)((double)pi0 * (double)pj0);
+    std::vector<float> pi_h((size_t)g.n_in, pi0), pj_h((size_t)g.n_out, pj0);
+
+    auto run = [&]() -> bcpnn_status {
+        HIP_TRY(L, hipMemcpyAsync(L->mask, mask.data(), hh, hipMemcpyHostToDevice, L->stream));
+        HIP_TRY(L, hipMemcpyAsync(L->act_list, list.data(), hh * sizeof(int32_t),
+                                  hipMemcpyHostToDevice, L->stream));
+        HIP_TRY(L, hipMemcpyAsync(L->act_count, count.data(), count.size() * sizeof(int32_t),
+                                  hipMemcpyHostToDevice, L->stream));
+        HIP_TRY(L, hipMemcpyAsync(L->pi[0], pi_h.data(), pi_h.size() * sizeof(float),
+                                  hipMemcpyHostToDevice, L->stream));
+        HIP_TRY(L, hipMemcpyAsync(L->pj[0], pj_h.data(), pj_h.size() * sizeof(float),
+                                  hipMemcpyHostToDevice, L->stream));
+        HIP_TRY(L, bcpnn::launch_init_state(L->stream, g, L->mask, pij0, cfg->init_noise, cfg->seed,
+                                            L->drop_bits, L->pij, L->w));
+        HIP_TRY(L, bcpnn::launch_bias(L->stream, g, L->pj[0], cfg->eps, cfg->bias_gain, L->b));
+        HIP_TRY(L, hipStreamSynchronize(L->stream));
+        return BCPNN_OK;
+    };
+    const bcpnn_status st = run();
+    if (st != BCPNN_OK) {
+        (void)hipStreamSynchronize(L->stream);
+        free_layer(L);
+        return st;
+    }
+    *out = L;
+    return BCPNN_OK;
+}
+
+void bcpnn_layer_destroy(bcpnn_layer* L) {
+    if (!L) return;
+    (void)hipStreamSynchronize(L->stream);
+    free_layer(L);
+}
+
+bcpnn_status bcpnn_forward(bcpnn_layer* L, const float* x_dev, int32_t B, float* y_dev,
+                           float* s_dev) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!x_dev || !y_dev) return fail(BCPNN_EINVAL, "x_dev and y_dev are required");
+    if (bcpnn_status st = check_batch(L, B)) return st;
+    HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
+                                     L->act_count, L->cfg.gain, 0, y_dev, s_dev, nullptr));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
+                               const float* target_dev, float* y_dev) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!x_dev) return fail(BCPNN_EINVAL, "x_dev is required");
+    if (bcpnn_status st = check_batch(L, B)) return st;
+    float* y = y_dev ? y_dev : L->y_buf;
+    HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
+                                     L->act_count, L->cfg.gain, 0, y, nullptr, nullptr));
+    const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
+    bcpnn::TraceArgs a;
+    a.x = x_dev;
+    a.t = target_dev ? target_dev : y;
+    a.B = B;
+    a.a_eff = (float)a_eff;
+    a.c1 = (float)(1.0 - a_eff);
+    a.inv_b = (float)(1.0 / B);
+    a.c2 = (float)(a_eff / B);
+    a.pi_old = L->pi[L->cur];
+    a.pj_old = L->pj[L->cur];
+    a.pi_new = L->pi[1 - L->cur];
+    a.pj_new = L->pj[1 - L->cur];
+    a.pij = L->pij;
+    a.w = L->w;
+    a.b = L->b;
+    a.mask = L->mask;
+    a.eps = L->cfg.eps;
+    a.bias_gain = L->cfg.bias_gain;
+    a.drop_bits = L->drop_bits;
+    std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
+    if (L->profiling) {
+        if (L->events_used == L->events.size()) {
+            std::pair<hipEvent_t, hipEvent_t> p;
+            HIP_TRY(L, hipEventCreate(&p.first));
+            HIP_TRY(L, hipEventCreate(&p.second));
+            L->events.push_back(p);
+        }
+        ev = &L->events[L->events_used++];
+        HIP_TRY(L, hipEventRecord(ev->first, L->stream));
+    }
+    HIP_TRY(L, bcpnn::launch_trace_update(L->stream, L->g, a));
+    if (ev) HIP_TRY(L, hipEventRecord(ev->second, L->stream));
+    L->cur = 1 - L->cur;
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_recompute_weights(bcpnn_layer* L) {
+    if (bcpnn_status st = usable(L)) return st;
+    HIP_TRY(L, bcpnn::launch_recompute_weights(L->stream, L->g, L->mask, L->pi[L->cur],
+                                               L->pj[L->cur], L->pij, L->cfg.eps,
+                                               L->cfg.bias_gain, L->drop_bits, L->w, L->b));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_structural_update(bcpnn_layer* L, int32_t* n_swapped_host) {
+    if (bcpnn_status st = usable(L)) return st;
+    HIP_TRY(L, bcpnn::launch_mutual_information(L->stream, L->g, L->pi[L->cur], L->pj[L->cur],
+                                                L->pij, L->cfg.eps, L->mi));
+    L->mi_valid = true;
+    if (L->cfg.n_swaps > 0)
+        HIP_TRY(L, bcpnn::launch_plasticity_swap(L->stream, L->g, L->mi, L->cfg.n_swaps,
+                                                 L->pi[L->cur], L->pj[L->cur], L->pij,
+                                                 L->cfg.eps, L->drop_bits, L->mask, L->w,
+                                                 L->act_list, L->act_count, L->swap_count));
+    if (n_swapped_host) {
+        *n_swapped_host = 0;
+        if (L->cfg.n_swaps > 0) {
+            std::vector<int32_t> c((size_t)L->cfg.out_hcu);
+            HIP_TRY(L, hipMemcpyAsync(c.data(), L->swap_count, c.size() * sizeof(int32_t),
+                                      hipMemcpyDeviceToHost, L->stream));
+            HIP_TRY(L, hipStreamSynchronize(L->stream));
+            for (int32_t v : c) *n_swapped_host += v;
+        }
+    }
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_readout(bcpnn_layer* L, const float* x_dev, int32_t B, int32_t* winner_dev) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!x_dev || !winner_dev) return fail(BCPNN_EINVAL, "x_dev and winner_dev are required");
+    if (bcpnn_status st = check_batch(L, B)) return st;
+    HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
+                                     L->act_count, L->cfg.gain, 1, nullptr, nullptr, winner_dev));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_get_state(const bcpnn_layer* Lc, const bcpnn_state_view* v) {
+    bcpnn_layer* L = const_cast<bcpnn_layer*>(Lc);
+    if (bcpnn_status st = usable(L)) return st;
+    if (!v) return fail(BCPNN_EINVAL, "view is NULL");
+    const Geometry& g = L->g;
+    const size_t E = (size_t)g.n_in * (size_t)g.n_out;
+    const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
+    auto d2h = [&](void* dst, const void* src, size_t bytes) {
+        return dst ? hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, L->stream) : hipSuccess;
+    };
+    HIP_TRY(L, d2h(v->pi, L->pi[L->cur], (size_t)g.n_in * sizeof(float)));
+    HIP_TRY(L, d2h(v->pj, L->pj[L->cur], (size_t)g.n_out * sizeof(float)));
+    HIP_TRY(L, d2h(v->pij, L->pij, E * sizeof(float)));
+    HIP_TRY(L, d2h(v->w, L->w, E * sizeof(float)));
+    HIP_TRY(L, d2h(v->b, L->b, (size_t)g.n_out * sizeof(float)));
+    HIP_TRY(L, d2h(v->mask, L->mask, hh));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!v || !v->pi || !v->pj || !v->pij || !v->w || !v->b || !v->mask)
+        return fail(BCPNN_EINVAL, "set_state needs all six arrays");
+    std::vector<int32_t> list, count;
+    if (const char* why = build_active_lists(L->cfg, v->mask, list, count))
+        return fail(BCPNN_EINVAL, "%s", why);
+    const Geometry& g = L->g;
+    const size_t E = (size_t)g.n_in * (size_t)g.n_out;
+    const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
+    HIP_TRY(L, hipMemcpyAsync(L->pi[L->cur], v->pi, (size_t)g.n_in * sizeof(float),
+                              hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->pj[L->cur], v->pj, (size_t)g.n_out * sizeof(float),
+                              hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->pij, v->pij, E * sizeof(float), hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->w, v->w, E * sizeof(float), hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->b, v->b, (size_t)g.n_out * sizeof(float), hipMemcpyHostToDevice,
+                              L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->mask, v->mask, hh, hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->act_list, list.data(), hh * sizeof(int32_t),
+                              hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, hipMemcpyAsync(L->act_count, count.data(), count.size() * sizeof(int32_t),
+                              hipMemcpyHostToDevice, L->stream));
+    HIP_TRY(L, bcpnn::launch_apply_mask(L->stream, g, L->mask, L->w));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    L->mi_valid = false;
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_get_mi(const bcpnn_layer* Lc, double* mi_host) {
+    bcpnn_layer* L = const_cast<bcpnn_layer*>(Lc);
+    if (bcpnn_status st = usable(L)) return st;
+    if (!mi_host) return fail(BCPNN_EINVAL, "mi_host is NULL");
+    if (!L->mi_valid) return fail(BCPNN_EINVAL, "no structural update since the state was set");
+    const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
+    HIP_TRY(L, hipMemcpyAsync(mi_host, L->mi, hh * sizeof(double), hipMemcpyDeviceToHost, L->stream));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_profile_enable(bcpnn_layer* L, int32_t enable) {
+    if (bcpnn_status st = usable(L)) return st;
+    L->profiling = enable != 0;
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_profile_read(bcpnn_layer* L, double* total_ms, int32_t* launches) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    double sum = 0.0;
+    for (size_t k = 0; k < L->events_used; ++k) {
+        float ms = 0.0f;
+        HIP_TRY(L, hipEventElapsedTime(&ms, L->events[k].first, L->events[k].second));
+        sum += ms;
+    }
+    *total_ms = sum;
+    *launches = (int32_t)L->events_used;
+    L->events_used = 0;
+    return BCPNN_OK;
+}
+
+}  // extern "C"

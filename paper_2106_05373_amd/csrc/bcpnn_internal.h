@@ -1,0 +1,84 @@
+// Internal declarations shared by the HIP translation units of libbcpnn (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bcpnn.h"
+
+namespace bcpnn {
+
+// Device-side description of the layer geometry and learning constants.
+struct Geometry {
+    int32_t in_hcu, in_mcu, out_hcu, out_mcu;
+    int64_t n_in, n_out;
+};
+
+// Storage rounding of Pij and W (bcpnn_storage): number of fp32 mantissa bits dropped.
+inline int storage_drop_bits(int32_t storage) {
+    return storage == BCPNN_STORE_BF16 ? 16 : (storage == BCPNN_STORE_M10 ? 13 : 0);
+}
+
+// ---- launchers (each enqueues on `stream` and returns hipGetLastError()) ----
+
+// Initial state: Pij = pij0, w = mask ? noise * (2u - 1) : 0 with u from SplitMix64.
+hipError_t launch_init_state(hipStream_t stream, const Geometry& g, const uint8_t* mask,
+                             float pij0, float init_noise, uint64_t seed, int drop_bits,
+                             float* pij, float* w);
+
+// b = bias_gain * log(max(pj, eps)).
+hipError_t launch_bias(hipStream_t stream, const Geometry& g, const float* pj, float eps,
+                       float bias_gain, float* b);
+
+// w = mask ? log(max(pij,eps) / (max(pi,eps) max(pj,eps))) : 0 over the whole matrix, and
+// b = bias_gain * log(max(pj, eps)).
+hipError_t launch_recompute_weights(hipStream_t stream, const Geometry& g, const uint8_t* mask,
+                                    const float* pi, const float* pj, const float* pij,
+                                    float eps, float bias_gain, int drop_bits, float* w,
+                                    float* b);
+
+// Zeroes the silent blocks of w (used after a host upload of w).
+hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_t* mask,
+                             float* w);
+
+// Support over the active input HCUs (fp64 MFMA) followed by, per (sample, hidden HCU):
+//   mode 0: softmax with gain -> y (and s if non-null);
+//   mode 1: argmax -> winner (and s if non-null).
+hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
+                          const float* w, const float* bias, const int32_t* act_list,
+                          const int32_t* act_count, float gain, int mode, float* y, float* s,
+                          int32_t* winner);
+
+// Joint-trace contraction with the fused trace, weight and bias updates:
+//   Pij <- c1 Pij + c2 sum_b x[b,i] t[b,j];  Pi, Pj from the batch means (read *_old, write
+//   *_new); w on active blocks; b = bias_gain log(max(Pj_new, eps)).
+struct TraceArgs {
+    const float* x;
+    const float* t;
+    int32_t B;
+    float c1, a_eff, inv_b, c2;
+    const float* pi_old;
+    const float* pj_old;
+    float* pi_new;
+    float* pj_new;
+    float* pij;
+    float* w;
+    float* b;
+    const uint8_t* mask;
+    float eps, bias_gain;
+    int drop_bits;
+};
+hipError_t launch_trace_update(hipStream_t stream, const Geometry& g, const TraceArgs& a);
+
+// Mutual information of every (input HCU, hidden HCU) block, fp64, [in_hcu][out_hcu].
+hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
+                                     const float* pj, const float* pij, float eps, double* mi);
+
+// Greedy swap per hidden HCU, patch of the swapped blocks of w, rebuild of the active lists.
+hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const double* mi,
+                                  int32_t n_swaps, const float* pi, const float* pj,
+                                  const float* pij, float eps, int drop_bits, uint8_t* mask,
+                                  float* w, int32_t* act_list, int32_t* act_count,
+                                  int32_t* swap_count);
+
+}  // namespace bcpnn

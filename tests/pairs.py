@@ -1,0 +1,126 @@
+"""Helpers that run the GPU library and the CPU oracle side by side on identical inputs.
+
+The GPU side goes through the C ABI (paper_2106_05373_amd.bcpnn); the oracle side through
+oracle/.  Only the seeded input generators (paper_2106_05373_amd.synth) serve both.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from paper_2106_05373_amd import synth
+
+# Tolerances (per step, from an identical prior state).
+TOL_ACT = 1e-5          # activities and traces, max-abs (fp32 storage)
+TOL_ACT_LOWP = 1e-2     # traces with bf16 / 10-bit-mantissa storage
+TOL_W = 1e-4            # weights and bias: |dw| <= TOL_W * max(1, |w|)
+# With reduced-precision storage both sides round w to the storage format; values computed
+# a few fp32 ulps apart can round to neighbouring storage values, one storage ulp apart:
+# 2^-7 relative for bf16 (7 stored mantissa bits), 2^-10 for the 10-bit format.
+TOL_W_STORAGE = {"f32": TOL_W, "bf16": 2.0 ** -7, "m10": 2.0 ** -10}
+TOL_S_REL = 1e-6        # support: fp64 sums on both sides, rounded to fp32 (<= a few ulp)
+TOL_MI_REL = 1e-12      # fp64 mutual information: summation order and libm differences
+
+
+def bcpnn():
+    """The GPU binding (imported lazily so CPU-only collection does not need the library)."""
+    from paper_2106_05373_amd import bcpnn as b
+    return b
+
+
+def gpu_config(in_hcu, in_mcu, out_hcu, out_mcu, max_batch, **kw):
+    return bcpnn().default_config(in_hcu, in_mcu, out_hcu, out_mcu, max_batch, **kw)
+
+
+def oracle_params(cfg) -> oracle.Params:
+    """Oracle parameters with the same values as a GPU config."""
+    return oracle.Params(cfg.in_hcu, cfg.in_mcu, cfg.out_hcu, cfg.out_mcu, cfg.alpha,
+                         cfg.n_cycles, cfg.gain, cfg.bias_gain, cfg.eps, cfg.pi_init,
+                         cfg.pj_init, cfg.init_noise, cfg.seed, cfg.n_swaps, cfg.storage)
+
+
+def workload_config(w: synth.Workload, max_batch=None, **kw):
+    L = w.layer
+    base = dict(alpha=w.alpha, gain=w.gain, init_noise=w.init_noise, seed=w.seed_noise,
+                storage=w.storage)
+    base.update(kw)
+    return gpu_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, max_batch or w.batch, **base)
+
+
+def workload_mask(w: synth.Workload) -> np.ndarray:
+    L = w.layer
+    if w.mask_frac >= 1.0:
+        return synth.full_mask(L.in_hcu, L.out_hcu)
+    return synth.random_mask(L.in_hcu, L.out_hcu, synth.active_count(L.in_hcu, w.mask_frac),
+                             w.seed_mask)
+
+
+class Pair:
+    """A GPU layer and an oracle layer created from one configuration and mask."""
+
+    def __init__(self, cfg, mask=None):
+        import torch
+        self.torch = torch
+        self.cfg = cfg
+        self.gpu = bcpnn().Layer(cfg, mask)
+        self.ora = oracle.OracleLayer(oracle_params(cfg), mask)
+        self.n_in, self.n_out = self.gpu.n_in, self.gpu.n_out
+
+    def dev(self, a, dtype=None):
+        t = self.torch
+        return t.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dtype or t.float32)
+
+    def sync_gpu_to_oracle(self):
+        """Give the GPU layer the oracle's exact state."""
+        self.gpu.set_state(self.ora.get_state())
+
+    def train(self, x, target=None):
+        """One batch on both sides; returns (y_gpu, y_oracle, s_oracle)."""
+        t = self.torch
+        xd = self.dev(x)
+        td = None if target is None else self.dev(target)
+        y = t.empty((x.shape[0], self.n_out), device="cuda", dtype=t.float32)
+        self.gpu.train_batch(xd, td, y)
+        s_o, y_o = self.ora.train_batch(x, target)
+        return y.cpu().numpy(), y_o, s_o
+
+    def forward(self, x):
+        t = self.torch
+        xd = self.dev(x)
+        y = t.empty((x.shape[0], self.n_out), device="cuda", dtype=t.float32)
+        s = t.empty_like(y)
+        self.gpu.forward(xd, y, s)
+        s_o, y_o = self.ora.forward(x)
+        return y.cpu().numpy(), s.cpu().numpy(), y_o, s_o
+
+    def close(self):
+        self.gpu.close()
+
+
+def max_abs(a, b):
+    return float(np.max(np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float64)))) if np.size(a) else 0.0
+
+
+def assert_weights_close(w_gpu, w_ora, what="w", tol=TOL_W):
+    w_gpu = np.asarray(w_gpu, np.float64)
+    w_ora = np.asarray(w_ora, np.float64)
+    err = np.abs(w_gpu - w_ora) / np.maximum(1.0, np.abs(w_ora))
+    assert err.max() <= tol, f"{what}: max scaled error {err.max():.3g} > {tol}"
+
+
+def assert_state_close(sg, so, tol=TOL_ACT, where="", storage="f32"):
+    for k in ("pi", "pj", "pij"):
+        e = max_abs(sg[k], so[k])
+        assert e <= tol, f"{where} {k}: max-abs {e:.3g} > {tol}"
+    assert_weights_close(sg["w"], so["w"], f"{where} w", TOL_W_STORAGE[storage])
+    assert_weights_close(sg["b"], so["b"], f"{where} b")
+    assert np.array_equal(sg["mask"], so["mask"]), f"{where} mask differs"
+
+
+def assert_support_close(s_gpu, s_ora):
+    s_gpu = np.asarray(s_gpu, np.float64)
+    s_ora = np.asarray(s_ora, np.float64)
+    err = np.abs(s_gpu - s_ora) / np.maximum(np.abs(s_ora), 1e-30)
+    small = np.abs(s_ora) < 1e-30
+    assert np.all(err[~small] <= TOL_S_REL), f"support: max rel error {err[~small].max():.3g}"
+    assert np.all(np.abs(s_gpu[small]) < 1e-30)

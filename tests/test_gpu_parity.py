@@ -1,0 +1,266 @@
+"""Parity of the HIP path (through the C ABI) against the CPU oracle, element by element.
+
+Every case feeds both sides the same seeded inputs.  Per-step cases start both sides from the
+same state (the oracle's, uploaded with set_state) and compare one call.  Tolerances are in
+tests/pairs.py: activities and traces max-abs 1e-5 (1e-2 with reduced-precision storage),
+weights and bias 1e-4 * max(1, |w|), support (fp64 sums on both sides) 1e-6 relative, MI
+1e-12 relative, masks and winners bit-exact.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2106_05373_amd import synth
+
+from pairs import (TOL_ACT, TOL_ACT_LOWP, TOL_MI_REL, Pair, assert_state_close,
+                   assert_support_close, assert_weights_close, gpu_config, max_abs,
+                   workload_config, workload_mask)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print(f"\n[gpu case] {request.node.nodeid}", flush=True)
+    yield
+
+
+def encoded(workload, n, split="train"):
+    px, labels = synth.dataset(workload, split=split, n=n)
+    return synth.encode_pixels(px), labels
+
+
+def pretrain(pair, X, steps, B, alpha=None):
+    """Moves the oracle to a non-trivial state (optionally with a faster rate), then copies it
+    to the GPU layer."""
+    p = pair.ora.p
+    saved = p.alpha
+    if alpha is not None:
+        p.alpha = alpha
+    for k in range(steps):
+        pair.ora.train_batch(X[(k * B) % (len(X) - B):][:B])
+    p.alpha = saved
+    pair.sync_gpu_to_oracle()
+
+
+TINY = synth.WORKLOADS["tiny"]
+MNIST = synth.WORKLOADS["mnist"]
+
+
+# ------------------------------------------------------------------------------------------
+def test_initial_state_matches_oracle():
+    for w in (TINY, MNIST):
+        pair = Pair(workload_config(w), workload_mask(w))
+        sg, so = pair.gpu.get_state(), pair.ora.get_state()
+        for k in ("pi", "pj", "pij", "w", "mask"):
+            assert np.array_equal(sg[k], so[k]), (w.name, k)
+        assert_weights_close(sg["b"], so["b"], "b")
+        pair.close()
+
+
+@pytest.mark.parametrize("B", [1, 13, 32, 100])
+def test_forward_matches_oracle(B):
+    X, _ = encoded(TINY, 512)
+    pair = Pair(workload_config(TINY, max_batch=128, gain=1.5), workload_mask(TINY))
+    pretrain(pair, X, 20, 32, alpha=0.05)
+    y, s, y_o, s_o = pair.forward(X[100:100 + B])
+    assert_support_close(s, s_o)
+    assert max_abs(y, y_o) <= TOL_ACT
+    pair.close()
+
+
+CASES = {
+    # name: (workload, config overrides, batch, target?)
+    "tiny": (TINY, {}, 32, False),
+    "tiny_ragged_13": (TINY, {}, 13, False),
+    "tiny_single_row": (TINY, {}, 1, False),
+    "tiny_gain0": (TINY, dict(gain=0.0), 32, False),
+    "tiny_gain3_cycles3": (TINY, dict(gain=3.0, n_cycles=3), 32, False),
+    "tiny_supervised": (TINY, {}, 32, True),
+    "tiny_bias_gain": (TINY, dict(bias_gain=0.5, eps=1e-4), 32, False),
+    "mnist_b128": (MNIST, {}, 128, False),
+    "mnist_b96_tail": (MNIST, {}, 96, False),
+    "mnist_bf16": (MNIST, dict(storage="bf16"), 128, False),
+    "mnist_m10": (MNIST, dict(storage="m10"), 128, False),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_one_step_matches_oracle(case):
+    w, over, B, supervised = CASES[case]
+    X, labels = encoded(w, 40 * B + B)
+    pair = Pair(workload_config(w, max_batch=max(B, w.batch), **over), workload_mask(w))
+    pretrain(pair, X, 30, B, alpha=0.05)
+    target = None
+    if supervised:
+        target = np.zeros((B, pair.n_out), np.float32)
+        for r in range(B):            # one-hot per hidden HCU from the sample's label
+            for h in range(pair.cfg.out_hcu):
+                target[r, h * pair.cfg.out_mcu + (labels[r] * 5 + h) % pair.cfg.out_mcu] = 1.0
+    x = X[-B:]
+    y, y_o, _ = pair.train(x, target)
+    storage = over.get("storage", "f32")
+    tol = TOL_ACT_LOWP if storage != "f32" else TOL_ACT
+    assert max_abs(y, y_o) <= TOL_ACT, f"y {max_abs(y, y_o)}"
+    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), tol=tol, where=case,
+                       storage=storage)
+    pair.close()
+
+
+def test_tiny_full_run_lockstep():
+    """The tiny workload end to end (2 epochs of 32 batches, per-epoch shuffles), the GPU
+    re-synchronised to the oracle before every batch: every batch's activities and state agree
+    to the per-step tolerance."""
+    w = TINY
+    X, _ = encoded(w, w.n_train)
+    pair = Pair(workload_config(w), workload_mask(w))
+    worst = 0.0
+    for e in range(w.epochs):
+        perm = synth.epoch_permutation(w.n_train, w.seed_shuffle, e)
+        for k in range(w.n_train // w.batch):
+            pair.sync_gpu_to_oracle()
+            y, y_o, _ = pair.train(X[perm[k * w.batch:(k + 1) * w.batch]])
+            worst = max(worst, max_abs(y, y_o))
+            assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where=f"e{e} b{k}")
+    print(f"worst per-batch activity error {worst:.3g}")
+    assert worst <= TOL_ACT
+    pair.close()
+
+
+def test_tiny_free_run_end_statistics():
+    """The same run without re-synchronising.  Rounding differences (fp32 kernels vs the fp64
+    oracle) feed back through the weights into the next batch's softmax, so the two
+    trajectories separate slowly; the end statistics must still agree: the winning MCU of every
+    (sample, hidden HCU) on a held-out pass, and the traces to 1e-4."""
+    w = TINY
+    X, _ = encoded(w, w.n_train)
+    pair = Pair(workload_config(w), workload_mask(w))
+    worst = 0.0
+    for e in range(w.epochs):
+        perm = synth.epoch_permutation(w.n_train, w.seed_shuffle, e)
+        for k in range(w.n_train // w.batch):
+            y, y_o, _ = pair.train(X[perm[k * w.batch:(k + 1) * w.batch]])
+            worst = max(worst, max_abs(y, y_o))
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    errs = {k: max_abs(sg[k], so[k]) for k in ("pi", "pj", "pij")}
+    y, _, y_o, _ = pair.forward(X[:32])
+    agree = float(np.mean(y.reshape(32, 4, 16).argmax(-1) == y_o.reshape(32, 4, 16).argmax(-1)))
+    print(f"free run: worst per-batch activity error {worst:.3g}, traces {errs}, "
+          f"winner agreement {agree:.4f}")
+    assert max(errs.values()) <= 1e-4
+    assert agree >= 0.99
+    pair.close()
+
+
+def test_structural_update_matches_oracle_bit_exactly():
+    w = MNIST
+    X, _ = encoded(w, 128 * 40)
+    pair = Pair(workload_config(w, n_swaps=2), workload_mask(w))
+    pretrain(pair, X, 40, 128, alpha=0.02)
+    n_gpu = pair.gpu.structural_update()
+    mi_gpu = pair.gpu.get_mi()
+    n_ora, mi_ora, _ = pair.ora.structural_update()
+    rel = np.abs(mi_gpu - mi_ora) / np.maximum(np.abs(mi_ora), 1e-300)
+    assert np.max(rel[mi_ora != 0]) <= TOL_MI_REL
+    assert n_gpu == n_ora and n_ora > 0
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    assert np.array_equal(sg["mask"], so["mask"])
+    assert_weights_close(sg["w"], so["w"])
+    # the decisions' smallest margin, for the record
+    srt = np.sort(mi_ora, axis=0)
+    gaps = np.diff(srt, axis=0)
+    print(f"swaps {n_ora}; smallest nonzero MI gap {gaps[gaps > 0].min():.3g}")
+    pair.close()
+
+
+def test_mnist_schedule_lockstep_with_plasticity():
+    """The MNIST-shaped workload's first 200 batches with its schedule (plasticity before
+    batches 100 and 200, 1-based), re-synchronising the GPU to the oracle after every batch:
+    every batch and both structural updates must agree."""
+    w = MNIST
+    X, _ = encoded(w, 128 * 200)
+    pair = Pair(workload_config(w), workload_mask(w))
+    swaps = []
+    for ib in range(1, 201):
+        if ib % w.period == 0:
+            pair.sync_gpu_to_oracle()
+            n_g = pair.gpu.structural_update()
+            n_o, _, _ = pair.ora.structural_update()
+            assert n_g == n_o
+            assert np.array_equal(pair.gpu.get_state(("mask",))["mask"], pair.ora.mask)
+            swaps.append(n_o)
+        pair.sync_gpu_to_oracle()
+        y, y_o, _ = pair.train(X[(ib - 1) * 128:ib * 128])
+        assert max_abs(y, y_o) <= TOL_ACT, f"batch {ib}: y {max_abs(y, y_o)}"
+        if ib % 50 == 0:
+            assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where=f"batch {ib}")
+    print(f"swaps per update {swaps}")
+    pair.close()
+
+
+def test_readout_matches_oracle():
+    w = MNIST
+    X, _ = encoded(w, 128 * 31)
+    pair = Pair(workload_config(w), workload_mask(w))
+    pretrain(pair, X, 30, 128, alpha=0.05)
+    t = pair.torch
+    x = X[-100:]
+    win = t.empty((100, pair.cfg.out_hcu), device="cuda", dtype=t.int32)
+    pair.gpu.readout(pair.dev(x), win)
+    np.testing.assert_array_equal(win.cpu().numpy(), pair.ora.readout(x))
+    pair.close()
+
+
+def test_recompute_weights_matches_oracle():
+    w = MNIST
+    X, _ = encoded(w, 128 * 11)
+    pair = Pair(workload_config(w), workload_mask(w))
+    pretrain(pair, X, 10, 128, alpha=0.05)
+    st = pair.ora.get_state()
+    st["w"] = np.zeros_like(st["w"])
+    st["b"] = np.zeros_like(st["b"])
+    pair.gpu.set_state(st)
+    pair.gpu.recompute_weights()
+    pair.ora.recompute_weights()
+    sg = pair.gpu.get_state()
+    assert_weights_close(sg["w"], pair.ora.w)
+    assert_weights_close(sg["b"], pair.ora.b)
+    pair.close()
+
+
+def test_runs_are_bitwise_deterministic():
+    w = MNIST
+    X, _ = encoded(w, 128 * 6)
+    mask = workload_mask(w)
+    states = []
+    for _ in range(2):
+        pair = Pair(workload_config(w, n_swaps=1), mask)
+        t = pair.torch
+        for k in range(6):
+            if k == 3:
+                pair.gpu.structural_update()
+            pair.gpu.train_batch(pair.dev(X[k * 128:(k + 1) * 128]))
+        states.append(pair.gpu.get_state())
+        pair.close()
+    for k in states[0]:
+        assert np.array_equal(states[0][k].view(np.uint8), states[1][k].view(np.uint8)), k
+
+
+def test_invalid_calls_are_rejected_and_change_nothing():
+    from paper_2106_05373_amd import bcpnn
+    w = TINY
+    pair = Pair(workload_config(w), workload_mask(w))
+    before = pair.gpu.get_state()
+    t = pair.torch
+    x = t.zeros((33, pair.n_in), device="cuda")
+    with pytest.raises(bcpnn.BcpnnError) as ei:
+        pair.gpu.train_batch(x)
+    assert ei.value.status == -1
+    st = dict(before)
+    st["mask"] = np.zeros_like(st["mask"])
+    with pytest.raises(bcpnn.BcpnnError):
+        pair.gpu.set_state(st)
+    after = pair.gpu.get_state()
+    for k in before:
+        assert np.array_equal(before[k], after[k]), k
+    pair.close()
