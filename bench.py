@@ -1,0 +1,212 @@
+"""Throughput of BCPNN hidden-layer training on one MI355X.
+
+Workload: the MNIST-shaped unsupervised layer -- 60000 synthetic 28x28 images encoded as 784
+input HCUs of 2 MCUs (x, 1 - x), a hidden layer of 30 HCUs x 100 MCUs with 10% receptive
+fields, batch 128, alpha 1e-3, structural plasticity before every 100th batch of an epoch
+(1-based), a fresh shuffle per epoch, the last batch of an epoch partial (96 samples).
+
+A step is one batch of that schedule: the structural update when it is due (MI score + greedy
+swap), then support, per-HCU softmax, trace, weight and bias updates.  The whole dataset, one
+shuffled copy per epoch touched, is staged in HBM before timing.  W warm-up steps run first;
+then exactly K steps are timed between two device synchronisations.
+
+Printed: one JSON line with the throughput (training samples/s), the roofline position of
+the dominant kernel (the joint-trace contraction, timed with HIP events on the layer's stream
+over the timed steps) and the CPU oracle's throughput on a bounded sample of the same
+schedule on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "train samples/s, MNIST-shaped 30x100 BCPNN layer; % MFMA peak, HBM GB/s"
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+# HBM traffic of the joint-trace kernel per launch (bytes), from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE runs scaled by the copy-kernel calibration factor, keyed by the SHA-256 of the
+# kernel source it was measured on.  A changed kernel reports null until measured again.
+MEASURED_TRAFFIC = {}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2345, help="timed batches (5 epochs = 2345)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="mnist", choices=["mnist", "stl"])
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="time budget of the CPU-oracle baseline sample (0 = skip)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def schedule(n_train, batch, period, n_steps):
+    """(epoch, batch index within epoch (0-based), start, size, plasticity-before?) per step."""
+    per_epoch = (n_train + batch - 1) // batch
+    out = []
+    for s in range(n_steps):
+        e, k = divmod(s, per_epoch)
+        start = k * batch
+        size = min(batch, n_train - start)
+        out.append((e, k, start, size, period > 0 and (k + 1) % period == 0))
+    return out
+
+
+def source_digest(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the "
+              "multi-GPU design is described in DESIGN.md and not run.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2106_05373_amd import bcpnn, synth
+
+    w = synth.WORKLOADS[args.workload]
+    L = w.layer
+    B = w.batch
+    n_steps = args.warmup + args.steps
+    sched = schedule(w.n_train, B, w.period, n_steps)
+    epochs = sorted({s[0] for s in sched})
+
+    # ---- data staged on the device (not timed) -----------------------------------------
+    t0 = time.time()
+    px, _ = synth.dataset(w)
+    X = torch.from_numpy(synth.encode_pixels(px))
+    del px
+    dev = torch.device("cuda", 0)
+    shuffled = {}
+    for e in epochs:
+        perm = torch.from_numpy(synth.epoch_permutation(w.n_train, w.seed_shuffle, e))
+        shuffled[e] = X[perm].to(dev).contiguous()
+    k_act = synth.active_count(L.in_hcu, w.mask_frac)
+    mask = synth.random_mask(L.in_hcu, L.out_hcu, k_act, w.seed_mask)
+    prep_s = time.time() - t0
+
+    stream = torch.cuda.Stream(device=dev)
+    cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
+                               gain=w.gain, init_noise=w.init_noise, seed=w.seed_noise)
+    layer = bcpnn.Layer(cfg, mask, stream=stream)
+
+    def step(s):
+        e, k, start, size, plastic = sched[s]
+        if plastic:
+            layer.structural_update(count=False)
+        layer.train_batch(shuffled[e][start:start + size])
+
+    torch.cuda.synchronize()
+    for s in range(args.warmup):
+        step(s)
+    torch.cuda.synchronize()
+
+    layer.profile_enable(True)
+    layer.profile_read()                          # discard anything recorded so far
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    ev0.record(stream)
+    for s in range(args.warmup, n_steps):
+        step(s)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    trace_ms, trace_launches = layer.profile_read()
+    layer.profile_enable(False)
+
+    wall_s = t_end - t_start
+    gpu_s = ev0.elapsed_time(ev1) / 1e3
+    samples = sum(sched[s][3] for s in range(args.warmup, n_steps))
+    plastic_steps = sum(sched[s][4] for s in range(args.warmup, n_steps))
+    value = samples / wall_s
+
+    # ---- roofline of the dominant kernel (joint-trace contraction + fused epilogue) ------
+    avg_trace_s = trace_ms / 1e3 / max(trace_launches, 1)
+    avg_b = samples / max(args.steps, 1)
+    flops_per_launch = 2.0 * L.n_in * L.n_out * avg_b
+    achieved_tflops = flops_per_launch / avg_trace_s / 1e12
+    digest = source_digest(os.path.join(ROOT, "paper_2106_05373_amd", "csrc", "k_trace.hip"))
+    traffic = MEASURED_TRAFFIC.get((args.workload, digest))
+    roofline = {
+        "bound": "mfma", "achieved": round(achieved_tflops, 3), "peak": PEAK_FP32_MFMA_TFLOPS,
+        "unit": "TFLOP/s", "frac": round(achieved_tflops / PEAK_FP32_MFMA_TFLOPS, 4),
+        "traffic": traffic,
+        "kernel": "trace_kernel (x^T y contraction, fp32 MFMA, fused trace/weight/bias epilogue)",
+        "avg_us": round(avg_trace_s * 1e6, 3), "launches": trace_launches,
+        "algorithmic_flops_per_launch": flops_per_launch,
+        "algorithmic_hbm_bytes_per_launch": 8.0 * L.n_in * L.n_out
+        + 4.0 * k_act * L.in_mcu * L.n_out,
+    }
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall_s * 1e3 / args.steps, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}: {w.n_train} synthetic images -> {L.in_hcu}x{L.in_mcu} inputs, "
+                        f"hidden {L.out_hcu} HCUs x {L.out_mcu} MCUs, "
+                        f"{int(round(w.mask_frac * 100))}% receptive fields, plasticity every "
+                        f"{w.period} batches, alpha {w.alpha}",
+            "global_batch": B, "samples_timed": samples, "structural_updates_timed": plastic_steps,
+            "gpu_event_s": round(gpu_s, 6), "wall_s": round(wall_s, 6),
+            "support_accumulation": "f64", "data_staging_s": round(prep_s, 2),
+            "parallelism": "single GPU",
+        },
+        "roofline": roofline,
+    }
+
+    if not args.no_cpu_baseline and args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, mask, shuffled, sched, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    layer.close()
+
+
+def cpu_baseline(w, mask, shuffled, sched, budget_s):
+    """The CPU oracle (as it stands) on the first batches of the same schedule, until the time
+    budget is spent; samples/s over the batches it finished."""
+    import oracle
+    L = w.layer
+    p = oracle.make_params(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, alpha=w.alpha, gain=w.gain,
+                           init_noise=w.init_noise, seed=w.seed_noise)
+    ora = oracle.OracleLayer(p, mask)
+    host = {e: None for e in shuffled}
+    for e in sorted(host)[:2]:                    # copies made before the clock starts
+        host[e] = shuffled[e].cpu().numpy()
+    done = samples = plastic = 0
+    t0 = time.perf_counter()
+    for (e, k, start, size, is_plastic) in sched:
+        if host[e] is None:
+            break
+        if is_plastic:
+            ora.structural_update()
+            plastic += 1
+        ora.train_batch(host[e][start:start + size])
+        done += 1
+        samples += size
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(samples / el, 2), "unit": "samples/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"first {done} batches ({samples} samples, {plastic} structural updates) "
+                      f"of the same schedule in {el:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

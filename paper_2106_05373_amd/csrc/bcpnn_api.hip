@@ -37,6 +37,7 @@ struct bcpnn_layer {
     Geometry g;
     hipStream_t stream = nullptr;
     int drop_bits = 0;
+    int32_t max_active = 0;              // largest active count of a hidden HCU (swaps keep it)
     float* pi[2] = {nullptr, nullptr};   // the trace kernel reads one and writes the other
     float* pj[2] = {nullptr, nullptr};
     int cur = 0;
@@ -75,7 +76,7 @@ const char* check_config(const bcpnn_config* c) {
     if (c->in_hcu > kMaxInHcu) return "in_hcu exceeds 49152";
     const int64_t n_in = (int64_t)c->in_hcu * c->in_mcu, n_out = (int64_t)c->out_hcu * c->out_mcu;
     if (n_in > (1ll << 31) - 1 || n_out > (1ll << 31) - 1) return "unit counts exceed 2^31 - 1";
-    if ((n_in + 127) / 128 > 65535) return "N_in exceeds 65535 * 128";
+    if ((n_in + 63) / 64 > 65535) return "N_in exceeds 65535 * 64";
     if (c->max_batch <= 0) return "max_batch must be positive";
     if (!(c->alpha > 0.0f && c->alpha <= 1.0f)) return "alpha must lie in (0, 1]";
     if (c->n_cycles < 1) return "n_cycles must be >= 1";
@@ -92,9 +93,11 @@ const char* check_config(const bcpnn_config* c) {
     return nullptr;
 }
 
-// Checks a host mask and builds the per-hidden-HCU active lists.
+// Checks a host mask and builds the per-hidden-HCU active lists; max_active receives the
+// largest count.
 const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
-                               std::vector<int32_t>& list, std::vector<int32_t>& count) {
+                               std::vector<int32_t>& list, std::vector<int32_t>& count,
+                               int32_t& max_active) {
     list.assign((size_t)c.out_hcu * c.in_hcu, 0);
     count.assign((size_t)c.out_hcu, 0);
     for (int32_t hi = 0; hi < c.in_hcu; ++hi)
@@ -103,8 +106,13 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
             if (m > 1) return "mask entries must be 0 or 1";
             if (m) list[(size_t)hj * c.in_hcu + count[hj]++] = hi;
         }
-    for (int32_t hj = 0; hj < c.out_hcu; ++hj)
+    max_active = 0;
+    for (int32_t hj = 0; hj < c.out_hcu; ++hj) {
         if (count[hj] == 0) return "every hidden HCU needs at least one active input HCU";
+        if (count[hj] > max_active) max_active = count[hj];
+    }
+    if ((int64_t)max_active * c.in_mcu > bcpnn::kMaxActiveUnits)
+        return "a hidden HCU has more than 12288 active input units (active HCUs * in_mcu)";
     return nullptr;
 }
 
@@ -172,10 +180,12 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     *out = nullptr;
     if (const char* why = check_config(cfg)) return fail(BCPNN_EINVAL, "%s", why);
     std::vector<int32_t> list, count;
-    if (const char* why = build_active_lists(*cfg, mask_host, list, count))
+    int32_t max_active = 0;
+    if (const char* why = build_active_lists(*cfg, mask_host, list, count, max_active))
         return fail(BCPNN_EINVAL, "%s", why);
 
     bcpnn_layer* L = new bcpnn_layer();
+    L->max_active = max_active;
     L->cfg = *cfg;
     L->g = Geometry{cfg->in_hcu, cfg->in_mcu, cfg->out_hcu, cfg->out_mcu,
                     (int64_t)cfg->in_hcu * cfg->in_mcu, (int64_t)cfg->out_hcu * cfg->out_mcu};
@@ -251,7 +261,8 @@ bcpnn_status bcpnn_forward(bcpnn_layer* L, const float* x_dev, int32_t B, float*
     if (!x_dev || !y_dev) return fail(BCPNN_EINVAL, "x_dev and y_dev are required");
     if (bcpnn_status st = check_batch(L, B)) return st;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
-                                     L->act_count, L->cfg.gain, 0, y_dev, s_dev, nullptr));
+                                     L->act_count, L->max_active, L->cfg.gain, 0, y_dev, s_dev,
+                                     nullptr));
     return BCPNN_OK;
 }
 
@@ -262,7 +273,8 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     if (bcpnn_status st = check_batch(L, B)) return st;
     float* y = y_dev ? y_dev : L->y_buf;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
-                                     L->act_count, L->cfg.gain, 0, y, nullptr, nullptr));
+                                     L->act_count, L->max_active, L->cfg.gain, 0, y, nullptr,
+                                     nullptr));
     const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
     bcpnn::TraceArgs a;
     a.x = x_dev;
@@ -336,7 +348,8 @@ bcpnn_status bcpnn_readout(bcpnn_layer* L, const float* x_dev, int32_t B, int32_
     if (!x_dev || !winner_dev) return fail(BCPNN_EINVAL, "x_dev and winner_dev are required");
     if (bcpnn_status st = check_batch(L, B)) return st;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
-                                     L->act_count, L->cfg.gain, 1, nullptr, nullptr, winner_dev));
+                                     L->act_count, L->max_active, L->cfg.gain, 1, nullptr,
+                                     nullptr, winner_dev));
     return BCPNN_OK;
 }
 
@@ -365,7 +378,8 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     if (!v || !v->pi || !v->pj || !v->pij || !v->w || !v->b || !v->mask)
         return fail(BCPNN_EINVAL, "set_state needs all six arrays");
     std::vector<int32_t> list, count;
-    if (const char* why = build_active_lists(L->cfg, v->mask, list, count))
+    int32_t max_active = 0;
+    if (const char* why = build_active_lists(L->cfg, v->mask, list, count, max_active))
         return fail(BCPNN_EINVAL, "%s", why);
     const Geometry& g = L->g;
     const size_t E = (size_t)g.n_in * (size_t)g.n_out;
@@ -385,6 +399,7 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
                               hipMemcpyHostToDevice, L->stream));
     HIP_TRY(L, bcpnn::launch_apply_mask(L->stream, g, L->mask, L->w));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
+    L->max_active = max_active;
     L->mi_valid = false;
     return BCPNN_OK;
 }

@@ -44,10 +44,15 @@ hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_
 // Support over the active input HCUs (fp64 MFMA) followed by, per (sample, hidden HCU):
 //   mode 0: softmax with gain -> y (and s if non-null);
 //   mode 1: argmax -> winner (and s if non-null).
+// max_active is the largest number of active input HCUs of any hidden HCU (swaps keep it).
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
-                          const int32_t* act_count, float gain, int mode, float* y, float* s,
-                          int32_t* winner);
+                          const int32_t* act_count, int32_t max_active, float gain, int mode,
+                          float* y, float* s, int32_t* winner);
+
+// Largest number of active input units (active HCUs * in_mcu) of one hidden HCU that the
+// support kernel keeps in its LDS unit table.
+constexpr int32_t kMaxActiveUnits = 12288;
 
 // Joint-trace contraction with the fused trace, weight and bias updates:
 //   Pij <- c1 Pij + c2 sum_b x[b,i] t[b,j];  Pi, Pj from the batch means (read *_old, write

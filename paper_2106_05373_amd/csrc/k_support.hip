@@ -10,11 +10,14 @@
 //    fp32, so every product is exact in fp64 and the sum's rounding error stays far below the
 //    fp32 rounding of the stored support.  (An fp32 accumulation of a few hundred terms of
 //    magnitude ~10 drifts by ~1e-5, the size of the tolerance on the activities.)
-//  * One workgroup owns one hidden HCU and 16 batch rows, i.e. complete softmax segments, so
-//    the softmax runs in the epilogue from LDS and the support never round-trips through HBM.
-//    Wave w computes the 16-column output tiles w, w + n_waves, ...; the 16 x K_h input panel
-//    is gathered into LDS once per chunk and shared by all waves; each weight row segment is
-//    read once per workgroup straight into the MFMA B operand.
+//  * One workgroup (8 waves) owns one hidden HCU and 16 batch rows, i.e. complete softmax
+//    segments, so the softmax runs in the epilogue from LDS and the support never round-trips
+//    through HBM.  Wave w computes the 16-column output tiles w, w + 8, ...
+//  * The K dimension is staged through LDS in chunks: the workgroup's weight rows (the active
+//    units' row segments, contiguous M_out floats each) and its 16 x K input panel are loaded
+//    cooperatively, all loads of a chunk in flight together, the next chunk into registers
+//    while the current one feeds the matrix cores.  The chunk is as large as the register and
+//    LDS budget allow (the whole K of the MNIST-shaped layer fits in one).
 //  * Work items (row tile, hidden HCU) are spread over the XCDs so that the row tiles of one
 //    hidden HCU share one XCD's L2 (they read the same weight block).
 //
@@ -28,94 +31,131 @@ namespace {
 
 typedef double d4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRows = 16;         // batch rows per workgroup
-constexpr int kChunk = 256;       // active input units staged per chunk
-constexpr int kMaxWaves = 8;
-constexpr int kTilesPerWave = 8;  // kMaxWaves * kTilesPerWave * 16 = 1024 = largest out_mcu
+constexpr int kRows = 16;          // batch rows per workgroup
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxTilesPerWave = 8;   // kWaves * 8 * 16 = 1024 = largest out_mcu
+// Weight elements staged per thread per chunk: fewer when the accumulators need the registers.
+constexpr int weight_regs(int tiles_per_wave) { return tiles_per_wave <= 2 ? 32 : 16; }
+constexpr int kXRegs = 8;          // input elements staged per thread per chunk
 
-__global__ void __launch_bounds__(64 * kMaxWaves)
-support_kernel(Geometry g, const float* __restrict__ x, int32_t B, const float* __restrict__ w,
-               const float* __restrict__ bias, const int32_t* __restrict__ act_list,
-               const int32_t* __restrict__ act_count, float gain, int mode, int n_tiles,
-               int mpad, int n_row_tiles, float* __restrict__ y, float* __restrict__ s,
+struct SupportLayout {
+    int n_tiles, mpad, n_row_tiles;
+    int kc;                        // units per chunk (multiple of 4)
+    int k_alloc;                   // LDS entries of the unit table (>= the largest K_h)
+    int xstride;                   // LDS row stride of the input panel (kc + 1: no bank aliasing)
+};
+
+// kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
+template <int kTilesPerWave>
+__global__ void __launch_bounds__(kThreads)
+support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32_t B,
+               const float* __restrict__ w, const float* __restrict__ bias,
+               const int32_t* __restrict__ act_list, const int32_t* __restrict__ act_count,
+               float gain, int mode, float* __restrict__ y, float* __restrict__ s,
                int32_t* __restrict__ winner) {
-    // LDS: the staged input panel during the contraction, the support tile afterwards.
     extern __shared__ float lds[];
-    float* xs = lds;                                            // [kRows][kChunk]
-    int32_t* units = reinterpret_cast<int32_t*>(lds + kRows * kChunk);   // [kChunk]
-    float* stile = lds;                                         // [kRows][mpad]
+    const int kc = lay.kc, mpad = lay.mpad, xstride = lay.xstride;
+    int32_t* units = reinterpret_cast<int32_t*>(lds);               // [k_alloc]
+    float* ws = lds + lay.k_alloc;                                   // [kc][mpad]
+    float* xs = ws + (size_t)kc * mpad;                              // [kRows][xstride]
+    float* stile = ws;                                               // [kRows][mpad] afterwards
 
-    const int64_t work = xcd_linear_index(blockIdx.x, (int64_t)n_row_tiles * g.out_hcu);
-    const int hj = (int)(work / n_row_tiles);
-    const int row0 = (int)(work % n_row_tiles) * kRows;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int n_waves = blockDim.x >> 6;
+    const int64_t work = xcd_linear_index(blockIdx.x, (int64_t)lay.n_row_tiles * g.out_hcu);
+    const int hj = (int)(work / lay.n_row_tiles);
+    const int row0 = (int)(work % lay.n_row_tiles) * kRows;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
 
-    const int64_t k_total = (int64_t)act_count[hj] * g.in_mcu;
+    const int32_t k_total = act_count[hj] * g.in_mcu;
     const int32_t* alist = act_list + (int64_t)hj * g.in_hcu;
     const int64_t col_base = (int64_t)hj * g.out_mcu;
+    for (int32_t k = tid; k < k_total; k += kThreads)
+        units[k] = alist[k / g.in_mcu] * g.in_mcu + k % g.in_mcu;
+    __syncthreads();
+
+    constexpr int kWRegs = weight_regs(kTilesPerWave);
+    const int w_elems = kc * g.out_mcu;
+    const int x_elems = kRows * kc;
+    float wr[kWRegs], xr[kXRegs];
+    auto load_chunk = [&](int32_t k0) {
+#pragma unroll
+        for (int q = 0; q < kWRegs; ++q) {
+            const int e = q * kThreads + tid;
+            const int u = e / g.out_mcu, c = e - u * g.out_mcu;
+            wr[q] = (e < w_elems && k0 + u < k_total)
+                        ? w[(int64_t)units[k0 + u] * g.n_out + col_base + c] : 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < kXRegs; ++q) {
+            const int e = q * kThreads + tid;
+            const int r = e / kc, u = e - r * kc;
+            xr[q] = (e < x_elems && k0 + u < k_total && row0 + r < B)
+                        ? x[(int64_t)(row0 + r) * g.n_in + units[k0 + u]] : 0.0f;
+        }
+    };
+    auto store_chunk = [&]() {
+#pragma unroll
+        for (int q = 0; q < kWRegs; ++q) {
+            const int e = q * kThreads + tid;
+            if (e < w_elems) {
+                const int u = e / g.out_mcu, c = e - u * g.out_mcu;
+                ws[u * mpad + c] = wr[q];
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kXRegs; ++q) {
+            const int e = q * kThreads + tid;
+            if (e < x_elems) {
+                const int r = e / kc, u = e - r * kc;
+                xs[r * xstride + u] = xr[q];
+            }
+        }
+    };
 
     d4 acc[kTilesPerWave];
 #pragma unroll
     for (int t = 0; t < kTilesPerWave; ++t) acc[t] = d4{0.0, 0.0, 0.0, 0.0};
 
-    for (int64_t k0 = 0; k0 < k_total; k0 += kChunk) {
-        const int kc = (int)((k_total - k0) < kChunk ? (k_total - k0) : kChunk);
-        __syncthreads();   // the previous chunk has been consumed
-        for (int t = threadIdx.x; t < kChunk; t += blockDim.x) {
-            int32_t unit = -1;
-            if (t < kc) {
-                const int64_t k = k0 + t;
-                unit = alist[k / g.in_mcu] * g.in_mcu + (int32_t)(k % g.in_mcu);
-            }
-            units[t] = unit;
-        }
+    if (k_total > 0) load_chunk(0);
+    for (int32_t k0 = 0; k0 < k_total; k0 += kc) {
+        __syncthreads();                          // the previous chunk has been consumed
+        store_chunk();
         __syncthreads();
-        for (int t = threadIdx.x; t < kRows * kChunk; t += blockDim.x) {
-            const int r = t / kChunk, c = t % kChunk;
-            const int32_t unit = units[c];
-            float v = 0.0f;
-            if (unit >= 0 && row0 + r < B) v = x[(int64_t)(row0 + r) * g.n_in + unit];
-            xs[t] = v;
-        }
-        __syncthreads();
-
-        const int ksteps = (kc + 3) / 4;
+        if (k0 + kc < k_total) load_chunk(k0 + kc);   // in flight during the MFMAs below
+        const int ksteps = (k_total - k0 < kc ? k_total - k0 + 3 : kc) / 4;
         for (int ks = 0; ks < ksteps; ++ks) {
             const int kk = ks * 4 + (lane >> 4);
-            const double a = (double)xs[(lane & 15) * kChunk + kk];
-            const int32_t unit = units[kk];
-            const float* wrow = w + (int64_t)(unit < 0 ? 0 : unit) * g.n_out + col_base;
+            const double av = (double)xs[(lane & 15) * xstride + kk];
 #pragma unroll
             for (int t = 0; t < kTilesPerWave; ++t) {
-                const int nt = wave + t * n_waves;
-                if (nt < n_tiles) {                       // uniform across the wave
-                    const int col = nt * 16 + (lane & 15);
-                    const double bv = (unit >= 0 && col < g.out_mcu) ? (double)wrow[col] : 0.0;
-                    acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, bv, acc[t], 0, 0, 0);
+                const int nt = wave + t * kWaves;
+                if (nt < lay.n_tiles) {           // uniform across the wave
+                    const double bv = (double)ws[kk * mpad + nt * 16 + (lane & 15)];
+                    acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[t], 0, 0, 0);
                 }
             }
         }
     }
 
-    __syncthreads();   // done with the input panel; reuse LDS for the support tile
+    __syncthreads();   // done with the panels; the support tile reuses their LDS
 #pragma unroll
     for (int t = 0; t < kTilesPerWave; ++t) {
-        const int nt = wave + t * n_waves;
-        if (nt < n_tiles) {
-            const int col = nt * 16 + (lane & 15);
-            if (col < g.out_mcu) {
-                const double bj = (double)bias[col_base + col];
+        const int nt = wave + t * kWaves;
+        if (nt < lay.n_tiles) {
+            const int c = nt * 16 + (lane & 15);
+            if (c < g.out_mcu) {
+                const double bj = (double)bias[col_base + c];
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    stile[((lane >> 4) + 4 * r) * mpad + col] = (float)(acc[t][r] + bj);
+                    stile[((lane >> 4) + 4 * r) * mpad + c] = (float)(acc[t][r] + bj);
             }
         }
     }
     __syncthreads();
 
-    for (int r = wave; r < kRows; r += n_waves) {
+    for (int r = wave; r < kRows; r += kWaves) {
         const int row = row0 + r;
         if (row >= B) break;                          // uniform across the wave
         const float* srow = stile + r * mpad;
@@ -146,24 +186,63 @@ support_kernel(Geometry g, const float* __restrict__ x, int32_t B, const float* 
     }
 }
 
+constexpr size_t kLdsBudget = 120 * 1024;
+
+SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k) {
+    SupportLayout L;
+    L.n_tiles = (g.out_mcu + 15) / 16;
+    const int kWRegs = weight_regs((L.n_tiles + kWaves - 1) / kWaves);
+    L.mpad = L.n_tiles * 16;
+    L.n_row_tiles = (B + kRows - 1) / kRows;
+    L.k_alloc = max_k > 0 ? max_k : 1;
+    const int by_regs_w = kWRegs * kThreads / g.out_mcu;
+    const int by_regs_x = kXRegs * kThreads / kRows;
+    const size_t fixed = (size_t)L.k_alloc * sizeof(int32_t);
+    const size_t per_unit = (size_t)L.mpad * sizeof(float) + (size_t)kRows * sizeof(float);
+    const int by_lds = (int)((kLdsBudget - fixed - kRows * sizeof(float)) / per_unit);
+    int kc = by_regs_w < by_regs_x ? by_regs_w : by_regs_x;
+    if (by_lds < kc) kc = by_lds;
+    const int need = (max_k + 3) & ~3;
+    if (need < kc) kc = need;
+    kc &= ~3;
+    L.kc = kc < 4 ? 4 : kc;
+    L.xstride = L.kc + 1;
+    return L;
+}
+
+size_t lds_bytes(const SupportLayout& L) {
+    const size_t panels = (size_t)L.k_alloc * sizeof(int32_t) +
+                          (size_t)L.kc * L.mpad * sizeof(float) +
+                          (size_t)kRows * L.xstride * sizeof(float);
+    const size_t tile = (size_t)L.k_alloc * sizeof(int32_t) + (size_t)kRows * L.mpad * sizeof(float);
+    return panels > tile ? panels : tile;
+}
+
 }  // namespace
 
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
-                          const int32_t* act_count, float gain, int mode, float* y, float* s,
-                          int32_t* winner) {
-    const int n_tiles = (g.out_mcu + 15) / 16;
-    const int mpad = n_tiles * 16;
-    const int n_waves = n_tiles < kMaxWaves ? n_tiles : kMaxWaves;
-    const int n_row_tiles = (B + kRows - 1) / kRows;
-    const size_t panel = (size_t)kRows * kChunk * sizeof(float) + kChunk * sizeof(int32_t);
-    const size_t tile = (size_t)kRows * mpad * sizeof(float);
-    const size_t lds = panel > tile ? panel : tile;
-    const int64_t blocks = (int64_t)n_row_tiles * g.out_hcu;
-    support_kernel<<<(unsigned)blocks, 64 * n_waves, lds, stream>>>(
-        g, x, B, w, bias, act_list, act_count, gain, mode, n_tiles, mpad, n_row_tiles, y, s,
-        winner);
-    return hipGetLastError();
+                          const int32_t* act_count, int32_t max_active, float gain, int mode,
+                          float* y, float* s, int32_t* winner) {
+    const SupportLayout lay = make_layout(g, B, max_active * g.in_mcu);
+    const size_t lds = lds_bytes(lay);
+    const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
+    const int64_t blocks = (int64_t)lay.n_row_tiles * g.out_hcu;
+    auto go = [&](auto kernel) {
+        if (lds > 64 * 1024) {
+            // allow dynamic LDS beyond 64 KB (gfx950 has 160 KB per workgroup)
+            (void)hipFuncSetAttribute((const void*)kernel,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            (void)hipGetLastError();
+        }
+        kernel<<<(unsigned)blocks, kThreads, lds, stream>>>(g, lay, x, B, w, bias, act_list,
+                                                            act_count, gain, mode, y, s, winner);
+        return hipGetLastError();
+    };
+    if (tpw <= 1) return go(support_kernel<1>);
+    if (tpw <= 2) return go(support_kernel<2>);
+    if (tpw <= 4) return go(support_kernel<4>);
+    return go(support_kernel<kMaxTilesPerWave>);
 }
 
 }  // namespace bcpnn

@@ -264,3 +264,108 @@ def test_invalid_calls_are_rejected_and_change_nothing():
     for k in before:
         assert np.array_equal(before[k], after[k]), k
     pair.close()
+
+
+SHAPES = {
+    # name: (in_hcu, in_mcu, out_hcu, out_mcu, active input HCUs per hidden HCU, batch)
+    "one_mcu_inputs": (50, 1, 5, 40, 50, 24),
+    "three_mcu_inputs": (40, 3, 6, 20, 17, 40),
+    "wide_200": (30, 2, 3, 200, 12, 33),          # two output tiles per wave
+    "wide_300": (30, 2, 2, 300, 30, 16),          # four
+    "wide_1024": (20, 2, 2, 1024, 7, 17),         # eight (the largest out_mcu)
+    "single_hidden_mcu": (25, 2, 40, 1, 5, 20),
+}
+
+
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_other_shapes_one_step(shape):
+    hin, min_, hout, mout, k, B = SHAPES[shape]
+    rng = np.random.default_rng(sum(map(ord, shape)))
+    mask = np.stack([synth.random_mask(hin, 1, k, 50 + c)[:, 0] for c in range(hout)], 1)
+    pair = Pair(gpu_config(hin, min_, hout, mout, B, alpha=0.05, gain=2.0), mask)
+    a = rng.random((20 * B, hin, min_)) + 0.05
+    X = (a / a.sum(-1, keepdims=True)).reshape(20 * B, -1).astype(np.float32)
+    pretrain(pair, X, 15, B, alpha=0.1)
+    y, s, y_o, s_o = pair.forward(X[:B])
+    assert_support_close(s, s_o)
+    assert max_abs(y, y_o) <= TOL_ACT
+    y, y_o, _ = pair.train(X[-B:])
+    assert max_abs(y, y_o) <= TOL_ACT
+    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where=shape)
+    if hout > 1 and k < hin:
+        pair.sync_gpu_to_oracle()
+        assert pair.gpu.structural_update() == pair.ora.structural_update()[0]
+        assert np.array_equal(pair.gpu.get_state(("mask",))["mask"], pair.ora.mask)
+    pair.close()
+
+
+def test_stl_shape_sampled():
+    """The STL-shaped layer at full size (55296 x 10000 traces, 5% receptive fields, batch 256)
+    in the launch configuration the benchmark uses: one structural update and one batch, checked
+    on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
+    from the GPU's prior weights, and the sampled blocks of the traces and weights from the
+    prior state restricted to the sampled input and hidden HCUs (the trace and weight updates
+    are elementwise given the batch, so a sub-problem reproduces them exactly)."""
+    w = synth.WORKLOADS["stl"]
+    Lw = w.layer
+    px, _ = synth.dataset(w, n=256)
+    x = synth.encode_pixels(px)
+    mask = workload_mask(w)
+    cfg = workload_config(w)
+    from pairs import bcpnn
+    t = __import__("torch")
+    layer = bcpnn().Layer(cfg, mask)
+    xd = t.from_numpy(x).cuda()
+    # a few batches move the state away from its initial product form
+    for _ in range(3):
+        layer.train_batch(xd)
+    prior = layer.get_state()
+    n = layer.structural_update()
+    after_swap = layer.get_state(("w", "mask"))
+    y = t.empty((256, Lw.n_out), device="cuda")
+    layer.train_batch(xd, None, y)
+    post = layer.get_state()
+    y = y.cpu().numpy()
+    rng = np.random.default_rng(7)
+
+    # structural update: MI of sampled blocks and the mask's per-HCU invariants
+    p_full = oracle_params_for(cfg)
+    assert (after_swap["mask"].sum(0) == mask.sum(0)).all()
+    assert n <= Lw.out_hcu
+    mi = layer.get_mi()
+    hi_s = rng.choice(Lw.in_hcu, 40, replace=False)
+    hj_s = rng.choice(Lw.out_hcu, 6, replace=False)
+    sub = sub_problem(prior, hi_s, hj_s, Lw)
+    mi_o = oracle.mutual_information(sub["p"], sub["pi"], sub["pj"], sub["pij"])
+    np.testing.assert_allclose(mi[np.ix_(hi_s, hj_s)], mi_o, rtol=TOL_MI_REL, atol=1e-15)
+    # activities of sampled rows: support recomputed from the post-swap weights
+    rows = rng.choice(256, 3, replace=False)
+    s_o = oracle.support(p_full, x[rows], after_swap["w"], prior["b"])
+    y_o = oracle.softmax(p_full, s_o)
+    assert max_abs(y[rows], y_o) <= TOL_ACT
+    # traces and weights of the sampled blocks
+    sub_post = sub_problem(post, hi_s, hj_s, Lw)
+    cols = sub["cols"]
+    pi, pj, pij = oracle.update_traces(sub["p"], x[:, sub["rows"]], y[:, cols], sub["pi"],
+                                       sub["pj"], sub["pij"])
+    assert max_abs(pij, sub_post["pij"]) <= TOL_ACT
+    assert max_abs(pi, sub_post["pi"]) <= TOL_ACT
+    m_sub = after_swap["mask"][np.ix_(hi_s, hj_s)]
+    w_o, _ = oracle.update_weights(sub["p"], m_sub, pi, pj, pij)
+    assert_weights_close(sub_post["w"], w_o)
+    layer.close()
+
+
+def oracle_params_for(cfg):
+    from pairs import oracle_params
+    return oracle_params(cfg)
+
+
+def sub_problem(st, hi_s, hj_s, Lw):
+    """The state restricted to the given input and hidden HCUs, as an oracle sub-layer."""
+    rows = (hi_s[:, None] * Lw.in_mcu + np.arange(Lw.in_mcu)).ravel()
+    cols = (hj_s[:, None] * Lw.out_mcu + np.arange(Lw.out_mcu)).ravel()
+    p = oracle.make_params(len(hi_s), Lw.in_mcu, len(hj_s), Lw.out_mcu, alpha=1e-3)
+    return dict(p=p, rows=rows, cols=cols, pi=st["pi"][rows], pj=st["pj"][cols],
+                pij=np.ascontiguousarray(st["pij"][np.ix_(rows, cols)]),
+                w=np.ascontiguousarray(st["w"][np.ix_(rows, cols)]))
