@@ -1,5 +1,6 @@
 // C ABI of libbcpnn (declared in include/bcpnn.h): argument checks, state ownership, launches.
 #include <math.h>
+#include <stdint.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -50,6 +51,7 @@ struct bcpnn_layer {
     int32_t* swap_count = nullptr;       // [out_hcu]
     double* mi = nullptr;                // [in_hcu][out_hcu]
     float* y_buf = nullptr;              // [max_batch][n_out] activity when the caller gives none
+    bcpnn::TraceOperands ops{};          // split batch operands of the joint-trace contraction
     bool mi_valid = false;
     bool failed = false;
     bool profiling = false;
@@ -119,7 +121,9 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
 void free_layer(bcpnn_layer* L) {
     if (!L) return;
     void* bufs[] = {L->pi[0], L->pi[1], L->pj[0], L->pj[1], L->pij, L->w, L->b, L->mask,
-                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf};
+                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf,
+                    L->ops.x_hi, L->ops.x_lo, L->ops.t_hi, L->ops.t_lo, L->ops.x_sum,
+                    L->ops.t_sum};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (auto& ev : L->events) {
@@ -140,6 +144,9 @@ bcpnn_status check_batch(const bcpnn_layer* L, int32_t B) {
         return fail(BCPNN_EINVAL, "batch %d outside [1, %d]", B, L->cfg.max_batch);
     return BCPNN_OK;
 }
+
+// Caller buffers are read and written with 16-byte vector accesses.
+bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 
 template <typename T>
 hipError_t dalloc(T** p, size_t n) {
@@ -209,6 +216,14 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = dalloc(&L->swap_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->mi, hh);
     if (e == hipSuccess) e = dalloc(&L->y_buf, (size_t)cfg->max_batch * g.n_out);
+    L->ops.kp = (cfg->max_batch + 31) / 32 * 32;
+    const size_t n_rt = (size_t)(cfg->max_batch + 15) / 16;
+    if (e == hipSuccess) e = dalloc(&L->ops.x_hi, (size_t)g.n_in * L->ops.kp);
+    if (e == hipSuccess) e = dalloc(&L->ops.x_lo, (size_t)g.n_in * L->ops.kp);
+    if (e == hipSuccess) e = dalloc(&L->ops.t_hi, (size_t)g.n_out * L->ops.kp);
+    if (e == hipSuccess) e = dalloc(&L->ops.t_lo, (size_t)g.n_out * L->ops.kp);
+    if (e == hipSuccess) e = dalloc(&L->ops.x_sum, n_rt * g.n_in);
+    if (e == hipSuccess) e = dalloc(&L->ops.t_sum, n_rt * g.n_out);
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,
@@ -259,10 +274,12 @@ bcpnn_status bcpnn_forward(bcpnn_layer* L, const float* x_dev, int32_t B, float*
                            float* s_dev) {
     if (bcpnn_status st = usable(L)) return st;
     if (!x_dev || !y_dev) return fail(BCPNN_EINVAL, "x_dev and y_dev are required");
+    if (misaligned(x_dev) || misaligned(y_dev) || misaligned(s_dev))
+        return fail(BCPNN_EINVAL, "device buffers must be 16-byte aligned");
     if (bcpnn_status st = check_batch(L, B)) return st;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 0, y_dev, s_dev,
-                                     nullptr));
+                                     nullptr, nullptr, nullptr));
     return BCPNN_OK;
 }
 
@@ -270,15 +287,16 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
                                const float* target_dev, float* y_dev) {
     if (bcpnn_status st = usable(L)) return st;
     if (!x_dev) return fail(BCPNN_EINVAL, "x_dev is required");
+    if (misaligned(x_dev) || misaligned(target_dev) || misaligned(y_dev))
+        return fail(BCPNN_EINVAL, "device buffers must be 16-byte aligned");
     if (bcpnn_status st = check_batch(L, B)) return st;
     float* y = y_dev ? y_dev : L->y_buf;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 0, y, nullptr,
-                                     nullptr));
+                                     nullptr, target_dev, &L->ops));
     const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
     bcpnn::TraceArgs a;
-    a.x = x_dev;
-    a.t = target_dev ? target_dev : y;
+    a.ops = L->ops;
     a.B = B;
     a.a_eff = (float)a_eff;
     a.c1 = (float)(1.0 - a_eff);
@@ -346,10 +364,12 @@ bcpnn_status bcpnn_structural_update(bcpnn_layer* L, int32_t* n_swapped_host) {
 bcpnn_status bcpnn_readout(bcpnn_layer* L, const float* x_dev, int32_t B, int32_t* winner_dev) {
     if (bcpnn_status st = usable(L)) return st;
     if (!x_dev || !winner_dev) return fail(BCPNN_EINVAL, "x_dev and winner_dev are required");
+    if (misaligned(x_dev) || misaligned(winner_dev))
+        return fail(BCPNN_EINVAL, "device buffers must be 16-byte aligned");
     if (bcpnn_status st = check_batch(L, B)) return st;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 1, nullptr,
-                                     nullptr, winner_dev));
+                                     nullptr, winner_dev, nullptr, nullptr));
     return BCPNN_OK;
 }
 

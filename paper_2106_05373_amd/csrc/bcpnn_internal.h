@@ -45,10 +45,22 @@ hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_
 //   mode 0: softmax with gain -> y (and s if non-null);
 //   mode 1: argmax -> winner (and s if non-null).
 // max_active is the largest number of active input HCUs of any hidden HCU (swaps keep it).
+// With ops non-null (training), the kernel also writes the contraction operands: the split
+// x^T from x, the split t^T from target (or from y when target is null), and the column sums.
+struct TraceOperands {
+    uint16_t* x_hi;   // [n_in][kp] bf16 bits
+    uint16_t* x_lo;
+    uint16_t* t_hi;   // [n_out][kp]
+    uint16_t* t_lo;
+    float* x_sum;     // [ceil(B / 16)][n_in]
+    float* t_sum;     // [ceil(B / 16)][n_out]
+    int32_t kp;       // row length (batch entries) of the split arrays, multiple of 32
+};
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
-                          float* y, float* s, int32_t* winner);
+                          float* y, float* s, int32_t* winner, const float* target,
+                          const TraceOperands* ops);
 
 // Largest number of active input units (active HCUs * in_mcu) of one hidden HCU that the
 // support kernel keeps in its LDS unit table.
@@ -56,10 +68,10 @@ constexpr int32_t kMaxActiveUnits = 12288;
 
 // Joint-trace contraction with the fused trace, weight and bias updates:
 //   Pij <- c1 Pij + c2 sum_b x[b,i] t[b,j];  Pi, Pj from the batch means (read *_old, write
-//   *_new); w on active blocks; b = bias_gain log(max(Pj_new, eps)).
+//   *_new); w on active blocks; b = bias_gain log(max(Pj_new, eps)).  The batch enters as the
+//   split operands and column sums written by the support kernel.
 struct TraceArgs {
-    const float* x;
-    const float* t;
+    TraceOperands ops;
     int32_t B;
     float c1, a_eff, inv_b, c2;
     const float* pi_old;

@@ -35,29 +35,65 @@ constexpr int kRows = 16;          // batch rows per workgroup
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxTilesPerWave = 8;   // kWaves * 8 * 16 = 1024 = largest out_mcu
-// Weight elements staged per thread per chunk: fewer when the accumulators need the registers.
-constexpr int weight_regs(int tiles_per_wave) { return tiles_per_wave <= 2 ? 32 : 16; }
-constexpr int kXRegs = 8;          // input elements staged per thread per chunk
+// Weight vectors staged per thread per chunk (each holds its own address while in flight).
+constexpr int stage_slots(int tiles_per_wave, int vec) {
+    // at least one widest row per thread: M_out <= 128 * tiles_per_wave, 32 lanes per row
+    return vec == 4 ? (tiles_per_wave >= 4 ? 8 : 12) : (tiles_per_wave >= 8 ? 32 : 16);
+}
+constexpr int kXRegs = 8;             // input elements staged per thread per chunk
+constexpr int kRowGroups = kThreads / 32;   // weight rows staged side by side (32 lanes each)
+static_assert(kRowGroups == kRows, "one row group per batch row of the input panel");
 
 struct SupportLayout {
     int n_tiles, mpad, n_row_tiles;
     int kc;                        // units per chunk (multiple of 4)
     int k_alloc;                   // LDS entries of the unit table (>= the largest K_h)
     int xstride;                   // LDS row stride of the input panel (kc + 1: no bank aliasing)
+    bool fits;                     // every thread's share of a chunk fits its staging slots
 };
 
+constexpr int kSplitCols = 128;   // input columns transposed per pass of the operand writer
+
+// Writes 16 consecutive batch entries of one column as bf16 hi and lo parts (hi = bf16(v),
+// lo = bf16(v - hi), round to nearest even), 32 bytes each; with pad, also 16 zero entries after.
+__device__ __forceinline__ void write_split_column(const float (&v)[kRows], uint16_t* hi,
+                                                   uint16_t* lo, bool pad) {
+    uint32_t h[kRows / 2], l[kRows / 2];
+#pragma unroll
+    for (int q = 0; q < kRows / 2; ++q) {
+        const __bf16 h0 = (__bf16)v[2 * q], h1 = (__bf16)v[2 * q + 1];
+        const __bf16 l0 = (__bf16)(v[2 * q] - (float)h0), l1 = (__bf16)(v[2 * q + 1] - (float)h1);
+        h[q] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+        l[q] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+    }
+    uint4* hp = reinterpret_cast<uint4*>(hi);
+    uint4* lp = reinterpret_cast<uint4*>(lo);
+    hp[0] = make_uint4(h[0], h[1], h[2], h[3]);
+    hp[1] = make_uint4(h[4], h[5], h[6], h[7]);
+    lp[0] = make_uint4(l[0], l[1], l[2], l[3]);
+    lp[1] = make_uint4(l[4], l[5], l[6], l[7]);
+    if (pad) {
+        const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+        hp[2] = z; hp[3] = z; lp[2] = z; lp[3] = z;
+    }
+}
+
 // kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
-template <int kTilesPerWave>
+// kVec: 4 when weight row segments can be read as float4 (M_out and N_out multiples of 4).
+template <int kTilesPerWave, int kVec>
 __global__ void __launch_bounds__(kThreads)
 support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32_t B,
                const float* __restrict__ w, const float* __restrict__ bias,
                const int32_t* __restrict__ act_list, const int32_t* __restrict__ act_count,
                float gain, int mode, float* __restrict__ y, float* __restrict__ s,
-               int32_t* __restrict__ winner) {
+               int32_t* __restrict__ winner, const float* __restrict__ target,
+               TraceOperands ops, int has_ops) {
+    typedef float vec_t __attribute__((ext_vector_type(kVec)));
+    constexpr int kSlots = stage_slots(kTilesPerWave, kVec);
     extern __shared__ float lds[];
     const int kc = lay.kc, mpad = lay.mpad, xstride = lay.xstride;
     int32_t* units = reinterpret_cast<int32_t*>(lds);               // [k_alloc]
-    float* ws = lds + lay.k_alloc;                                   // [kc][mpad]
+    float* ws = lds + ((lay.k_alloc + 3) & ~3);                      // [kc][mpad]
     float* xs = ws + (size_t)kc * mpad;                              // [kRows][xstride]
     float* stile = ws;                                               // [kRows][mpad] afterwards
 
@@ -67,6 +103,8 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
+    const int sub = tid & 31;          // lane within a row group
+    const int grp = tid >> 5;          // row group
 
     const int32_t k_total = act_count[hj] * g.in_mcu;
     const int32_t* alist = act_list + (int64_t)hj * g.in_hcu;
@@ -75,48 +113,66 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
         units[k] = alist[k / g.in_mcu] * g.in_mcu + k % g.in_mcu;
     __syncthreads();
 
-    constexpr int kWRegs = weight_regs(kTilesPerWave);
-    const int w_elems = kc * g.out_mcu;
-    const int x_elems = kRows * kc;
-    float wr[kWRegs], xr[kXRegs];
+    // Weight rows: row group grp takes chunk rows grp, grp + 16, ...; its 32 lanes take the
+    // vectors sub, sub + 32, ... of each row.  Input panel: row r = grp, units sub, sub + 32, ...
+    const int nvec = g.out_mcu / kVec;
+    vec_t wr[kSlots];
+    float xr[kXRegs];
+    // Each thread walks its weight slots in a fixed order: rows grp, grp + 16, ..., and within
+    // a row the vectors sub, sub + 32, ... below nvec (lanes with sub >= nvec stay idle).  The
+    // walk is unrolled over the slots, so every load of a chunk is issued before any is used.
     auto load_chunk = [&](int32_t k0) {
+        int u = grp, v = sub;
 #pragma unroll
-        for (int q = 0; q < kWRegs; ++q) {
-            const int e = q * kThreads + tid;
-            const int u = e / g.out_mcu, c = e - u * g.out_mcu;
-            wr[q] = (e < w_elems && k0 + u < k_total)
-                        ? w[(int64_t)units[k0 + u] * g.n_out + col_base + c] : 0.0f;
+        for (int q = 0; q < kSlots; ++q) {
+            wr[q] = vec_t(0.0f);
+            if (v < nvec && u < kc && k0 + u < k_total) {
+                const vec_t* src =
+                    reinterpret_cast<const vec_t*>(w + (int64_t)units[k0 + u] * g.n_out + col_base);
+                wr[q] = src[v];
+            }
+            v += 32;
+            if (v >= nvec) { v = sub; u += kRowGroups; }
         }
+        const int64_t xrow = (int64_t)(row0 + grp) * g.n_in;
+        const bool rok = row0 + grp < B;
 #pragma unroll
         for (int q = 0; q < kXRegs; ++q) {
-            const int e = q * kThreads + tid;
-            const int r = e / kc, u = e - r * kc;
-            xr[q] = (e < x_elems && k0 + u < k_total && row0 + r < B)
-                        ? x[(int64_t)(row0 + r) * g.n_in + units[k0 + u]] : 0.0f;
+            const int uu = sub + 32 * q;
+            xr[q] = (rok && uu < kc && k0 + uu < k_total) ? x[xrow + units[k0 + uu]] : 0.0f;
         }
     };
     auto store_chunk = [&]() {
+        int u = grp, v = sub;
 #pragma unroll
-        for (int q = 0; q < kWRegs; ++q) {
-            const int e = q * kThreads + tid;
-            if (e < w_elems) {
-                const int u = e / g.out_mcu, c = e - u * g.out_mcu;
-                ws[u * mpad + c] = wr[q];
-            }
+        for (int q = 0; q < kSlots; ++q) {
+            if (v < nvec && u < kc) reinterpret_cast<vec_t*>(ws + u * mpad)[v] = wr[q];
+            v += 32;
+            if (v >= nvec) { v = sub; u += kRowGroups; }
         }
 #pragma unroll
         for (int q = 0; q < kXRegs; ++q) {
-            const int e = q * kThreads + tid;
-            if (e < x_elems) {
-                const int r = e / kc, u = e - r * kc;
-                xs[r * xstride + u] = xr[q];
-            }
+            const int uu = sub + 32 * q;
+            if (uu < kc) xs[grp * xstride + uu] = xr[q];
         }
     };
 
-    d4 acc[kTilesPerWave];
+    // With one tile per wave, two accumulator chains (even and odd k-steps) keep consecutive
+    // MFMAs independent; with more tiles, the tiles do.
+    constexpr int kChains = kTilesPerWave == 1 ? 2 : 1;
+    d4 acc[kChains][kTilesPerWave];
 #pragma unroll
-    for (int t = 0; t < kTilesPerWave; ++t) acc[t] = d4{0.0, 0.0, 0.0, 0.0};
+    for (int c = 0; c < kChains; ++c)
+#pragma unroll
+        for (int t = 0; t < kTilesPerWave; ++t) acc[c][t] = d4{0.0, 0.0, 0.0, 0.0};
+    // Output tile t of this wave is wave + 8 t; a wave with fewer tiles than kTilesPerWave
+    // repeats its last valid one (same reads, result discarded), so the loop has no branches.
+    int col_of[kTilesPerWave];
+#pragma unroll
+    for (int t = 0; t < kTilesPerWave; ++t) {
+        const int nt = wave + t * kWaves;
+        col_of[t] = (nt < lay.n_tiles ? nt : lay.n_tiles - 1) * 16 + (lane & 15);
+    }
 
     if (k_total > 0) load_chunk(0);
     for (int32_t k0 = 0; k0 < k_total; k0 += kc) {
@@ -124,17 +180,30 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
         store_chunk();
         __syncthreads();
         if (k0 + kc < k_total) load_chunk(k0 + kc);   // in flight during the MFMAs below
-        const int ksteps = (k_total - k0 < kc ? k_total - k0 + 3 : kc) / 4;
-        for (int ks = 0; ks < ksteps; ++ks) {
+        // k-steps of 4 units (the rows beyond k_total hold zeros): groups of 8, then the rest
+        const int rem = k_total - k0 < kc ? k_total - k0 : kc;
+        const int ksteps = (rem + 3) / 4;
+        int ks = 0;
+        for (; ks + 8 <= ksteps; ks += 8) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int kk = (ks + u) * 4 + (lane >> 4);
+                const double av = (double)xs[(lane & 15) * xstride + kk];
+#pragma unroll
+                for (int t = 0; t < kTilesPerWave; ++t) {
+                    const double bv = (double)ws[kk * mpad + col_of[t]];
+                    acc[u % kChains][t] =
+                        __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[u % kChains][t], 0, 0, 0);
+                }
+            }
+        }
+        for (; ks < ksteps; ++ks) {
             const int kk = ks * 4 + (lane >> 4);
             const double av = (double)xs[(lane & 15) * xstride + kk];
 #pragma unroll
             for (int t = 0; t < kTilesPerWave; ++t) {
-                const int nt = wave + t * kWaves;
-                if (nt < lay.n_tiles) {           // uniform across the wave
-                    const double bv = (double)ws[kk * mpad + nt * 16 + (lane & 15)];
-                    acc[t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[t], 0, 0, 0);
-                }
+                const double bv = (double)ws[kk * mpad + col_of[t]];
+                acc[0][t] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[0][t], 0, 0, 0);
             }
         }
     }
@@ -149,55 +218,147 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
                 const double bj = (double)bias[col_base + c];
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    stile[((lane >> 4) + 4 * r) * mpad + c] = (float)(acc[t][r] + bj);
+                {
+                    double v = acc[0][t][r];
+                    if constexpr (kChains == 2) v += acc[1][t][r];
+                    stile[((lane >> 4) + 4 * r) * mpad + c] = (float)(v + bj);
+                }
             }
         }
     }
     __syncthreads();
 
-    for (int r = wave; r < kRows; r += kWaves) {
-        const int row = row0 + r;
-        if (row >= B) break;                          // uniform across the wave
-        const float* srow = stile + r * mpad;
-        const int64_t out = (int64_t)row * g.n_out + col_base;
-        if (s)
-            for (int m = lane; m < g.out_mcu; m += 64) s[out + m] = srow[m];
-        if (mode == 0) {
-            float mx = -INFINITY;
-            for (int m = lane; m < g.out_mcu; m += 64) mx = fmaxf(mx, srow[m]);
-            mx = wave_max(mx);
-            float den = 0.0f;
-            for (int m = lane; m < g.out_mcu; m += 64) den += expf(gain * (srow[m] - mx));
-            den = wave_sum(den);
-            const float inv = 1.0f / den;
-            for (int m = lane; m < g.out_mcu; m += 64) y[out + m] = expf(gain * (srow[m] - mx)) * inv;
-        } else {
-            float bv = -INFINITY;
-            int bi = 0x7fffffff;
-            for (int m = lane; m < g.out_mcu; m += 64)
-                if (srow[m] > bv) { bv = srow[m]; bi = m; }
-            for (int off = 32; off > 0; off >>= 1) {
-                const float ov = __shfl_xor(bv, off, 64);
-                const int oi = __shfl_xor(bi, off, 64);
-                if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+    // Each wave takes rows wave and wave + 8 together (independent reduction chains).
+    static_assert(kRows == 2 * kWaves, "two softmax rows per wave");
+    {
+        const int ra = wave, rb = wave + kWaves;
+        const bool va = row0 + ra < B, vb = row0 + rb < B;
+        float* sa = stile + ra * mpad;
+        float* sb = stile + rb * mpad;
+        const int64_t oa = (int64_t)(row0 + ra) * g.n_out + col_base;
+        const int64_t ob = (int64_t)(row0 + rb) * g.n_out + col_base;
+        if (s) {
+            for (int m = lane; m < g.out_mcu; m += 64) {
+                if (va) s[oa + m] = sa[m];
+                if (vb) s[ob + m] = sb[m];
             }
-            if (lane == 0) winner[(int64_t)row * g.out_hcu + hj] = bi;
+        }
+        if (mode == 0) {
+            float ma = -INFINITY, mb = -INFINITY;
+            for (int m = lane; m < g.out_mcu; m += 64) {
+                ma = fmaxf(ma, sa[m]);
+                mb = fmaxf(mb, sb[m]);
+            }
+            for (int off = 32; off > 0; off >>= 1) {
+                ma = fmaxf(ma, __shfl_xor(ma, off, 64));
+                mb = fmaxf(mb, __shfl_xor(mb, off, 64));
+            }
+            float da = 0.0f, db = 0.0f;
+            for (int m = lane; m < g.out_mcu; m += 64) {
+                const float ea = expf(gain * (sa[m] - ma));
+                const float eb = expf(gain * (sb[m] - mb));
+                sa[m] = ea;
+                sb[m] = eb;
+                da += ea;
+                db += eb;
+            }
+            for (int off = 32; off > 0; off >>= 1) {
+                da += __shfl_xor(da, off, 64);
+                db += __shfl_xor(db, off, 64);
+            }
+            const float ia = 1.0f / da, ib = 1.0f / db;
+            for (int m = lane; m < g.out_mcu; m += 64) {
+                const float ya = sa[m] * ia, yb = sb[m] * ib;
+                sa[m] = ya;                           // kept for the contraction operands
+                sb[m] = yb;
+                if (va) y[oa + m] = ya;
+                if (vb) y[ob + m] = yb;
+            }
+        } else {
+            float bva = -INFINITY, bvb = -INFINITY;
+            int bia = 0x7fffffff, bib = 0x7fffffff;
+            for (int m = lane; m < g.out_mcu; m += 64) {
+                if (sa[m] > bva) { bva = sa[m]; bia = m; }
+                if (sb[m] > bvb) { bvb = sb[m]; bib = m; }
+            }
+            for (int off = 32; off > 0; off >>= 1) {
+                const float ova = __shfl_xor(bva, off, 64), ovb = __shfl_xor(bvb, off, 64);
+                const int oia = __shfl_xor(bia, off, 64), oib = __shfl_xor(bib, off, 64);
+                if (ova > bva || (ova == bva && oia < bia)) { bva = ova; bia = oia; }
+                if (ovb > bvb || (ovb == bvb && oib < bib)) { bvb = ovb; bib = oib; }
+            }
+            if (lane == 0) {
+                if (va) winner[(int64_t)(row0 + ra) * g.out_hcu + hj] = bia;
+                if (vb) winner[(int64_t)(row0 + rb) * g.out_hcu + hj] = bib;
+            }
+        }
+    }
+    if (!has_ops) return;
+
+    // Contraction operands of this workgroup's share of the batch (rows row0 .. row0 + 15):
+    // the hidden HCU's columns of t (the activity above, or the target) and the input columns
+    // [c0, c1) of x, each column split into bf16 hi / lo parts and written transposed, plus the
+    // column sums over these rows.  The last row tile also clears the rows up to the next
+    // multiple of 32, so the contraction can run over whole 32-row chunks.
+    const int rows = B - row0 < kRows ? B - row0 : kRows;
+    const int n_rt = lay.n_row_tiles;
+    const int rt = row0 / kRows;
+    const bool pad = rt == n_rt - 1 && (n_rt & 1);   // round_up(B, 32) = (n_rt + 1) * 16
+    __syncthreads();
+    for (int m = tid; m < g.out_mcu; m += kThreads) {
+        float v[kRows];
+        float sum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            v[r] = r < rows ? (target ? target[(int64_t)(row0 + r) * g.n_out + col_base + m]
+                                      : stile[r * mpad + m])
+                            : 0.0f;
+            sum += v[r];
+        }
+        const int64_t col = col_base + m;
+        write_split_column(v, ops.t_hi + col * ops.kp + row0, ops.t_lo + col * ops.kp + row0, pad);
+        ops.t_sum[(int64_t)rt * g.n_out + col] = sum;
+    }
+    const int64_t c0 = (int64_t)hj * g.n_in / g.out_hcu;
+    const int64_t c1 = (int64_t)(hj + 1) * g.n_in / g.out_hcu;
+    float* xt = stile;                                           // [kRows][kSplitCols]
+    for (int64_t cb = c0; cb < c1; cb += kSplitCols) {
+        __syncthreads();
+        for (int e = tid; e < kRows * kSplitCols; e += kThreads) {
+            const int r = e / kSplitCols, cc = e % kSplitCols;
+            xt[e] = (r < rows && cb + cc < c1) ? x[(int64_t)(row0 + r) * g.n_in + cb + cc] : 0.0f;
+        }
+        __syncthreads();
+        for (int cc = tid; cc < kSplitCols && cb + cc < c1; cc += kThreads) {
+            float v[kRows];
+            float sum = 0.0f;
+#pragma unroll
+            for (int r = 0; r < kRows; ++r) {
+                v[r] = xt[r * kSplitCols + cc];
+                sum += v[r];
+            }
+            const int64_t i = cb + cc;
+            write_split_column(v, ops.x_hi + i * ops.kp + row0, ops.x_lo + i * ops.kp + row0, pad);
+            ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
         }
     }
 }
 
 constexpr size_t kLdsBudget = 120 * 1024;
 
-SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k) {
+SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) {
     SupportLayout L;
     L.n_tiles = (g.out_mcu + 15) / 16;
-    const int kWRegs = weight_regs((L.n_tiles + kWaves - 1) / kWaves);
     L.mpad = L.n_tiles * 16;
     L.n_row_tiles = (B + kRows - 1) / kRows;
     L.k_alloc = max_k > 0 ? max_k : 1;
-    const int by_regs_w = kWRegs * kThreads / g.out_mcu;
-    const int by_regs_x = kXRegs * kThreads / kRows;
-    const size_t fixed = (size_t)L.k_alloc * sizeof(int32_t);
+    // chunk rows such that every thread holds at most `slots` weight vectors
+    const int vec_per_row = (g.out_mcu / vec + 31) / 32;
+    const int tpw = (L.n_tiles + kWaves - 1) / kWaves;
+    const int slots = stage_slots(tpw <= 1 ? 1 : tpw <= 2 ? 2 : tpw <= 4 ? 4 : kMaxTilesPerWave, vec);
+    const int by_regs_w = kRowGroups * (slots / vec_per_row);
+    const int by_regs_x = 32 * kXRegs;
+    const size_t fixed = (size_t)((L.k_alloc + 3) & ~3) * sizeof(int32_t);
     const size_t per_unit = (size_t)L.mpad * sizeof(float) + (size_t)kRows * sizeof(float);
     const int by_lds = (int)((kLdsBudget - fixed - kRows * sizeof(float)) / per_unit);
     int kc = by_regs_w < by_regs_x ? by_regs_w : by_regs_x;
@@ -205,17 +366,23 @@ SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k) {
     const int need = (max_k + 3) & ~3;
     if (need < kc) kc = need;
     kc &= ~3;
-    L.kc = kc < 4 ? 4 : kc;
+    if (kc < 4) kc = 4;
+    // every thread must hold its share of a chunk: ceil(kc / 16) rows x vec_per_row vectors
+    while (kc > 4 && ((kc + kRowGroups - 1) / kRowGroups) * vec_per_row > slots) kc -= 4;
+    L.kc = kc;
     L.xstride = L.kc + 1;
+    L.fits = ((kc + kRowGroups - 1) / kRowGroups) * vec_per_row <= slots;
     return L;
 }
 
 size_t lds_bytes(const SupportLayout& L) {
-    const size_t panels = (size_t)L.k_alloc * sizeof(int32_t) +
-                          (size_t)L.kc * L.mpad * sizeof(float) +
+    const size_t table = (size_t)((L.k_alloc + 3) & ~3) * sizeof(int32_t);
+    const size_t panels = (size_t)L.kc * L.mpad * sizeof(float) +
                           (size_t)kRows * L.xstride * sizeof(float);
-    const size_t tile = (size_t)L.k_alloc * sizeof(int32_t) + (size_t)kRows * L.mpad * sizeof(float);
-    return panels > tile ? panels : tile;
+    size_t tile = (size_t)kRows * L.mpad * sizeof(float);
+    const size_t split = (size_t)kRows * kSplitCols * sizeof(float);
+    if (split > tile) tile = split;
+    return table + (panels > tile ? panels : tile);
 }
 
 }  // namespace
@@ -223,8 +390,11 @@ size_t lds_bytes(const SupportLayout& L) {
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
-                          float* y, float* s, int32_t* winner) {
-    const SupportLayout lay = make_layout(g, B, max_active * g.in_mcu);
+                          float* y, float* s, int32_t* winner, const float* target,
+                          const TraceOperands* ops) {
+    const int vec = (g.out_mcu % 4 == 0 && g.n_out % 4 == 0) ? 4 : 1;
+    const SupportLayout lay = make_layout(g, B, max_active * g.in_mcu, vec);
+    if (!lay.fits) return hipErrorInvalidValue;
     const size_t lds = lds_bytes(lay);
     const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
     const int64_t blocks = (int64_t)lay.n_row_tiles * g.out_hcu;
@@ -235,14 +405,22 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
             (void)hipGetLastError();
         }
+        const TraceOperands o = ops ? *ops : TraceOperands{};
         kernel<<<(unsigned)blocks, kThreads, lds, stream>>>(g, lay, x, B, w, bias, act_list,
-                                                            act_count, gain, mode, y, s, winner);
+                                                            act_count, gain, mode, y, s, winner,
+                                                            target, o, ops ? 1 : 0);
         return hipGetLastError();
     };
-    if (tpw <= 1) return go(support_kernel<1>);
-    if (tpw <= 2) return go(support_kernel<2>);
-    if (tpw <= 4) return go(support_kernel<4>);
-    return go(support_kernel<kMaxTilesPerWave>);
+    if (vec == 4) {
+        if (tpw <= 1) return go(support_kernel<1, 4>);
+        if (tpw <= 2) return go(support_kernel<2, 4>);
+        if (tpw <= 4) return go(support_kernel<4, 4>);
+        return go(support_kernel<kMaxTilesPerWave, 4>);
+    }
+    if (tpw <= 1) return go(support_kernel<1, 1>);
+    if (tpw <= 2) return go(support_kernel<2, 1>);
+    if (tpw <= 4) return go(support_kernel<4, 1>);
+    return go(support_kernel<kMaxTilesPerWave, 1>);
 }
 
 }  // namespace bcpnn
