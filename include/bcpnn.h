@@ -63,16 +63,20 @@ typedef enum {
 typedef enum { BCPNN_STORE_F32 = 0, BCPNN_STORE_BF16 = 1, BCPNN_STORE_M10 = 2 } bcpnn_storage;
 
 typedef struct {
-    int32_t in_hcu, in_mcu;     /* input HCUs and MCUs per HCU (> 0)                          */
-    int32_t out_hcu, out_mcu;   /* hidden HCUs and MCUs per HCU (> 0, out_mcu <= 1024)         */
-    int32_t max_batch;          /* largest B accepted by forward/train_batch/readout (> 0)    */
+    int32_t in_hcu, in_mcu;     /* input HCUs and MCUs per HCU (> 0, in_hcu <= 49152,
+                                   N_in <= 65535 * 64)                                       */
+    int32_t out_hcu, out_mcu;   /* hidden HCUs and MCUs per HCU (> 0, out_mcu <= 1024,
+                                   N_out <= 2^22)                                            */
+    int32_t max_batch;          /* largest B accepted by forward/train_batch/readout,
+                                   in [1, 2^20]                                              */
     float alpha;                /* trace rate l of Alg. 1, in (0, 1]; from a time constant
                                    tau (in batches) use alpha = 1 / tau                      */
     int32_t n_cycles;           /* repetitions of the trace/weight cycle per batch (>= 1);
                                    equivalent to one cycle at 1 - (1 - alpha)^n_cycles        */
     float gain;                 /* softmax gain g (>= 0, finite); 1 is the paper's softmax    */
     float bias_gain;            /* k_B of Alg. 1 (finite)                                     */
-    float eps;                  /* lower clamp of each probability inside a log (> 0)         */
+    float eps;                  /* lower clamp of each probability inside a log (a normal
+                                   float: FLT_MIN <= eps, finite)                            */
     float pi_init, pj_init;     /* initial Pi, Pj; <= 0 selects 1 / in_mcu, 1 / out_mcu        */
     float init_noise;           /* initial w = mask * init_noise * (2u - 1), u ~ U[0, 1) from
                                    the SplitMix64 finaliser of (seed, i * N_out + j)          */
@@ -143,9 +147,10 @@ bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in
  * to the host.  Waits.  EINVAL before the first structural update. */
 bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
 
-/* Kernel timing for measurement: while enabled, the library records HIP events on its stream
- * around every launch of the joint-trace kernel.  bcpnn_profile_read waits for the stream and
- * returns the summed duration (ms) and count of the launches since the last read. */
+/* Kernel timing for measurement: while enabled, every launch of the joint-trace kernel carries
+ * a pair of HIP events stamped by the dispatch itself (hipExtLaunchKernel), so they bracket the
+ * kernel's execution alone.  bcpnn_profile_read waits for the stream and returns the summed
+ * duration (ms) and count of the launches since the last read. */
 bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t enable);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
 

@@ -1,4 +1,5 @@
 // C ABI of libbcpnn (declared in include/bcpnn.h): argument checks, state ownership, launches.
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdarg.h>
@@ -79,12 +80,13 @@ const char* check_config(const bcpnn_config* c) {
     const int64_t n_in = (int64_t)c->in_hcu * c->in_mcu, n_out = (int64_t)c->out_hcu * c->out_mcu;
     if (n_in > (1ll << 31) - 1 || n_out > (1ll << 31) - 1) return "unit counts exceed 2^31 - 1";
     if ((n_in + 63) / 64 > 65535) return "N_in exceeds 65535 * 64";
-    if (c->max_batch <= 0) return "max_batch must be positive";
+    if (n_out > (1ll << 22)) return "N_out exceeds 2^22";      // a 64-row Pij tile < 2^30 bytes
+    if (c->max_batch <= 0 || c->max_batch > (1 << 20)) return "max_batch must lie in [1, 2^20]";
     if (!(c->alpha > 0.0f && c->alpha <= 1.0f)) return "alpha must lie in (0, 1]";
     if (c->n_cycles < 1) return "n_cycles must be >= 1";
     if (!(c->gain >= 0.0f) || !isfinite(c->gain)) return "gain must be finite and >= 0";
     if (!isfinite(c->bias_gain)) return "bias_gain must be finite";
-    if (!(c->eps > 0.0f) || !isfinite(c->eps)) return "eps must be finite and > 0";
+    if (!(c->eps >= FLT_MIN) || !isfinite(c->eps)) return "eps must be a finite normal float > 0";
     if (!isfinite(c->pi_init) || !isfinite(c->pj_init) || c->pi_init > 1.0f || c->pj_init > 1.0f)
         return "pi_init / pj_init must be finite and <= 1";
     if (!isfinite(c->init_noise) || c->init_noise < 0.0f) return "init_noise must be finite and >= 0";
@@ -322,10 +324,9 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
             L->events.push_back(p);
         }
         ev = &L->events[L->events_used++];
-        HIP_TRY(L, hipEventRecord(ev->first, L->stream));
     }
-    HIP_TRY(L, bcpnn::launch_trace_update(L->stream, L->g, a));
-    if (ev) HIP_TRY(L, hipEventRecord(ev->second, L->stream));
+    HIP_TRY(L, bcpnn::launch_trace_update(L->stream, L->g, a, ev ? ev->first : nullptr,
+                                          ev ? ev->second : nullptr));
     L->cur = 1 - L->cur;
     return BCPNN_OK;
 }

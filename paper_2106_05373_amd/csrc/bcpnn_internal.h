@@ -85,7 +85,9 @@ struct TraceArgs {
     float eps, bias_gain;
     int drop_bits;
 };
-hipError_t launch_trace_update(hipStream_t stream, const Geometry& g, const TraceArgs& a);
+// start / stop (nullable) receive the kernel's own start and end time stamps.
+hipError_t launch_trace_update(hipStream_t stream, const Geometry& g, const TraceArgs& a,
+                               hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 // Mutual information of every (input HCU, hidden HCU) block, fp64, [in_hcu][out_hcu].
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,

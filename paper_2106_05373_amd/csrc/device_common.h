@@ -26,6 +26,12 @@ __device__ __forceinline__ float log_ratio(float pij, float pi, float pj, float 
     return __logf(fmaxf(pij, eps) / den);
 }
 
+// Natural log through the hardware base-2 log (v_log_f32, about one ulp for normal inputs)
+// times ln 2; callers pass normal floats only (every argument here is clamped to eps >= FLT_MIN).
+__device__ __forceinline__ float fast_log(float x) {
+    return __builtin_amdgcn_logf(x) * 0.6931471805599453f;
+}
+
 // Uniform draw in [0, 1) with 24 bits: the SplitMix64 output function (Steele, Lea, Flood,
 // OOPSLA 2014) applied to state seed + (idx + 1) * golden-ratio increment.
 __device__ __forceinline__ float splitmix_uniform(uint64_t seed, uint64_t idx) {

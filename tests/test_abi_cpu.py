@@ -53,7 +53,10 @@ BAD = {
     "cycles 0": dict(n_cycles=0),
     "negative gain": dict(gain=-1.0),
     "eps 0": dict(eps=0.0),
+    "eps subnormal": dict(eps=1e-40),
     "max_batch 0": dict(max_batch=0),
+    "max_batch above 2^20": dict(max_batch=(1 << 20) + 1),
+    "N_out above 2^22": dict(out_hcu=(1 << 22) // 1024 + 1, out_mcu=1024),
     "swaps negative": dict(n_swaps=-1),
     "swaps too many": dict(n_swaps=257),
     "storage unknown": dict(storage=7),
