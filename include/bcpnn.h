@@ -147,11 +147,14 @@ bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in
  * to the host.  Waits.  EINVAL before the first structural update. */
 bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
 
-/* Kernel timing for measurement: while enabled, every launch of the joint-trace kernel carries
- * a pair of HIP events stamped by the dispatch itself (hipExtLaunchKernel), so they bracket the
- * kernel's execution alone.  bcpnn_profile_read waits for the stream and returns the summed
- * duration (ms) and count of the launches since the last read. */
-bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t enable);
+/* Kernel timing for measurement: with period n > 0, every n-th launch of the joint-trace kernel
+ * (counting from the call) carries a pair of HIP events stamped by the dispatch itself
+ * (hipExtLaunchKernel), so they bracket the kernel's execution alone; n = 0 turns it off.  Each
+ * timed launch costs the stream a few microseconds of dispatch, so a period of 10 or more
+ * keeps a throughput measurement nearly unperturbed.  bcpnn_profile_read waits for the stream
+ * and returns the summed duration (ms) and count of the timed launches since the last read.
+ * Errors: EINVAL for n < 0. */
+bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
 
 /* Message of the calling thread's last failure ("" if none). */

@@ -231,8 +231,9 @@ class Layer:
         return mi
 
     # -- measurement -----------------------------------------------------------------------
-    def profile_enable(self, on: bool = True):
-        _check(lib.bcpnn_profile_enable(self._h, int(on)))
+    def profile_enable(self, period: int = 1):
+        """Time every period-th joint-trace launch with dispatch-stamped events (0 = off)."""
+        _check(lib.bcpnn_profile_enable(self._h, int(period)))
 
     def profile_read(self):
         """(total ms, launches) of the joint-trace kernel since the last read."""

@@ -55,7 +55,8 @@ struct bcpnn_layer {
     bcpnn::TraceOperands ops{};          // split batch operands of the joint-trace contraction
     bool mi_valid = false;
     bool failed = false;
-    bool profiling = false;
+    int32_t profile_every = 0;           // 0: off; n: every n-th trace launch carries events
+    int64_t trace_launches = 0;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
     size_t events_used = 0;
 };
@@ -218,14 +219,22 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = dalloc(&L->swap_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->mi, hh);
     if (e == hipSuccess) e = dalloc(&L->y_buf, (size_t)cfg->max_batch * g.n_out);
-    L->ops.kp = (cfg->max_batch + 31) / 32 * 32;
-    const size_t n_rt = (size_t)(cfg->max_batch + 15) / 16;
-    if (e == hipSuccess) e = dalloc(&L->ops.x_hi, (size_t)g.n_in * L->ops.kp);
-    if (e == hipSuccess) e = dalloc(&L->ops.x_lo, (size_t)g.n_in * L->ops.kp);
-    if (e == hipSuccess) e = dalloc(&L->ops.t_hi, (size_t)g.n_out * L->ops.kp);
-    if (e == hipSuccess) e = dalloc(&L->ops.t_lo, (size_t)g.n_out * L->ops.kp);
+    // split operands in fragment order: 1 KiB per 32 units and 16 batch rows; the units past
+    // the layer in the last block are never written and must read as zero
+    L->ops.n_ks = (cfg->max_batch + 15) / 16;
+    const size_t n_rt = (size_t)L->ops.n_ks;
+    const size_t xf = (size_t)((g.n_in + 31) / 32) * n_rt * 512;
+    const size_t tf = (size_t)((g.n_out + 31) / 32) * n_rt * 512;
+    if (e == hipSuccess) e = dalloc(&L->ops.x_hi, xf);
+    if (e == hipSuccess) e = dalloc(&L->ops.x_lo, xf);
+    if (e == hipSuccess) e = dalloc(&L->ops.t_hi, tf);
+    if (e == hipSuccess) e = dalloc(&L->ops.t_lo, tf);
     if (e == hipSuccess) e = dalloc(&L->ops.x_sum, n_rt * g.n_in);
     if (e == hipSuccess) e = dalloc(&L->ops.t_sum, n_rt * g.n_out);
+    if (e == hipSuccess) e = hipMemsetAsync(L->ops.x_hi, 0, xf * sizeof(uint16_t), L->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(L->ops.x_lo, 0, xf * sizeof(uint16_t), L->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(L->ops.t_hi, 0, tf * sizeof(uint16_t), L->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(L->ops.t_lo, 0, tf * sizeof(uint16_t), L->stream);
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,
@@ -316,7 +325,7 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     a.bias_gain = L->cfg.bias_gain;
     a.drop_bits = L->drop_bits;
     std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
-    if (L->profiling) {
+    if (L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
         if (L->events_used == L->events.size()) {
             std::pair<hipEvent_t, hipEvent_t> p;
             HIP_TRY(L, hipEventCreate(&p.first));
@@ -438,7 +447,9 @@ bcpnn_status bcpnn_get_mi(const bcpnn_layer* Lc, double* mi_host) {
 
 bcpnn_status bcpnn_profile_enable(bcpnn_layer* L, int32_t enable) {
     if (bcpnn_status st = usable(L)) return st;
-    L->profiling = enable != 0;
+    if (enable < 0) return fail(BCPNN_EINVAL, "profile period must be >= 0");
+    L->profile_every = enable;
+    L->trace_launches = 0;
     return BCPNN_OK;
 }
 

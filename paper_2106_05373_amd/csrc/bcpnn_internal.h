@@ -47,15 +47,26 @@ hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_
 // max_active is the largest number of active input HCUs of any hidden HCU (swaps keep it).
 // With ops non-null (training), the kernel also writes the contraction operands: the split
 // x^T from x, the split t^T from target (or from y when target is null), and the column sums.
+// The contraction operands are stored in MFMA fragment order: per block of 32 units and k-step of
+// 16 batch rows, 64 lanes x 8 bf16 (1 KiB), lane l holding rows 8 (l / 32) .. + 7 of unit
+// l % 32 -- exactly the A / B operand of v_mfma_f32_32x32x16_bf16, so a wave loads one step of
+// one operand as a single contiguous 1 KiB read.  Units past the layer stay zero.
 struct TraceOperands {
-    uint16_t* x_hi;   // [n_in][kp] bf16 bits
+    uint16_t* x_hi;   // [ceil(n_in / 32)][n_ks][64][8] bf16 bits
     uint16_t* x_lo;
-    uint16_t* t_hi;   // [n_out][kp]
+    uint16_t* t_hi;   // [ceil(n_out / 32)][n_ks][64][8]
     uint16_t* t_lo;
     float* x_sum;     // [ceil(B / 16)][n_in]
     float* t_sum;     // [ceil(B / 16)][n_out]
-    int32_t kp;       // row length (batch entries) of the split arrays, multiple of 32
+    int32_t n_ks;     // k-steps per unit block: ceil(max_batch / 16)
 };
+
+// Element offset (bf16 units) of the fragment chunk that holds batch rows 8 h .. 8 h + 7 of unit
+// u in k-step ks (16 bytes, 8 consecutive rows).
+__host__ __device__ inline int64_t frag_chunk(int64_t u, int64_t ks, int h, int32_t n_ks) {
+    return (((u >> 5) * n_ks + ks) * 64 + (u & 31) + 32 * h) * 8;
+}
+
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,

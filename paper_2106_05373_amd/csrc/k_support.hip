@@ -54,10 +54,10 @@ struct SupportLayout {
 
 constexpr int kSplitCols = 128;   // input columns transposed per pass of the operand writer
 
-// Writes 16 consecutive batch entries of one column as bf16 hi and lo parts (hi = bf16(v),
-// lo = bf16(v - hi), round to nearest even), 32 bytes each; with pad, also 16 zero entries after.
+// Writes the 16 batch entries of unit u in k-step ks (one row tile) as bf16 hi and lo parts
+// (hi = bf16(v), lo = bf16(v - hi), round to nearest even): two 16-byte fragment chunks each.
 __device__ __forceinline__ void write_split_column(const float (&v)[kRows], uint16_t* hi,
-                                                   uint16_t* lo, bool pad) {
+                                                   uint16_t* lo, int64_t u, int ks, int32_t n_ks) {
     uint32_t h[kRows / 2], l[kRows / 2];
 #pragma unroll
     for (int q = 0; q < kRows / 2; ++q) {
@@ -66,16 +66,11 @@ __device__ __forceinline__ void write_split_column(const float (&v)[kRows], uint
         h[q] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
         l[q] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
     }
-    uint4* hp = reinterpret_cast<uint4*>(hi);
-    uint4* lp = reinterpret_cast<uint4*>(lo);
-    hp[0] = make_uint4(h[0], h[1], h[2], h[3]);
-    hp[1] = make_uint4(h[4], h[5], h[6], h[7]);
-    lp[0] = make_uint4(l[0], l[1], l[2], l[3]);
-    lp[1] = make_uint4(l[4], l[5], l[6], l[7]);
-    if (pad) {
-        const uint4 z = make_uint4(0u, 0u, 0u, 0u);
-        hp[2] = z; hp[3] = z; lp[2] = z; lp[3] = z;
-    }
+    const int64_t c0 = frag_chunk(u, ks, 0, n_ks), c1 = frag_chunk(u, ks, 1, n_ks);
+    *reinterpret_cast<uint4*>(hi + c0) = make_uint4(h[0], h[1], h[2], h[3]);
+    *reinterpret_cast<uint4*>(hi + c1) = make_uint4(h[4], h[5], h[6], h[7]);
+    *reinterpret_cast<uint4*>(lo + c0) = make_uint4(l[0], l[1], l[2], l[3]);
+    *reinterpret_cast<uint4*>(lo + c1) = make_uint4(l[4], l[5], l[6], l[7]);
 }
 
 // kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
@@ -295,15 +290,12 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     }
     if (!has_ops) return;
 
-    // Contraction operands of this workgroup's share of the batch (rows row0 .. row0 + 15):
-    // the hidden HCU's columns of t (the activity above, or the target) and the input columns
-    // [c0, c1) of x, each column split into bf16 hi / lo parts and written transposed, plus the
-    // column sums over these rows.  The last row tile also clears the rows up to the next
-    // multiple of 32, so the contraction can run over whole 32-row chunks.
+    // Contraction operands of this workgroup's share of the batch (rows row0 .. row0 + 15, one
+    // k-step): the hidden HCU's columns of t (the activity above, or the target) and the input
+    // columns [c0, c1) of x, each column split into bf16 hi / lo parts and written in fragment
+    // order, plus the column sums over these rows.  Rows past B are written as zeros.
     const int rows = B - row0 < kRows ? B - row0 : kRows;
-    const int n_rt = lay.n_row_tiles;
     const int rt = row0 / kRows;
-    const bool pad = rt == n_rt - 1 && (n_rt & 1);   // round_up(B, 32) = (n_rt + 1) * 16
     __syncthreads();
     for (int m = tid; m < g.out_mcu; m += kThreads) {
         float v[kRows];
@@ -316,7 +308,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             sum += v[r];
         }
         const int64_t col = col_base + m;
-        write_split_column(v, ops.t_hi + col * ops.kp + row0, ops.t_lo + col * ops.kp + row0, pad);
+        write_split_column(v, ops.t_hi, ops.t_lo, col, rt, ops.n_ks);
         ops.t_sum[(int64_t)rt * g.n_out + col] = sum;
     }
     const int64_t c0 = (int64_t)hj * g.n_in / g.out_hcu;
@@ -338,7 +330,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
                 sum += v[r];
             }
             const int64_t i = cb + cc;
-            write_split_column(v, ops.x_hi + i * ops.kp + row0, ops.x_lo + i * ops.kp + row0, pad);
+            write_split_column(v, ops.x_hi, ops.x_lo, i, rt, ops.n_ks);
             ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
         }
     }
