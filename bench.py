@@ -49,10 +49,17 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2345, help="timed batches (5 epochs = 2345)")
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="mnist", choices=["mnist", "stl"])
+    ap.add_argument("--workload", default="mnist", choices=["mnist", "stl", "mnist_pipeline"],
+                    help="mnist / stl: hidden-layer training (the metric); mnist_pipeline: the "
+                         "hidden layer plus a supervised readout, then held-out inference")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle baseline sample (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--precision-report", action="store_true",
+                    help="reduced-precision storage: f32 / bf16 / 10-bit-mantissa layers against "
+                         "the fp32 oracle over one epoch (trace, weight and hidden-code error)")
+    ap.add_argument("--inference-sweep", action="store_true",
+                    help="forward-pass throughput of the MNIST-shaped layer over batch sizes")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 256 MiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -90,6 +97,13 @@ def main():
         print(json.dumps({"calibration": "copy", "bytes_read": src.numel() * 4,
                           "bytes_written": dst.numel() * 4, "launches": 5}))
         return
+
+    if args.workload == "mnist_pipeline":
+        return run_pipeline(args)
+    if args.precision_report:
+        return run_precision_report(args)
+    if args.inference_sweep:
+        return run_inference_sweep(args)
 
     w = synth.WORKLOADS[args.workload]
     L = w.layer
@@ -196,6 +210,222 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, mask, shuffled, sched, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     layer.close()
+
+
+def run_pipeline(args):
+    """Hidden layer (3 epochs, plasticity) + supervised 1 x 10 readout (1 epoch), then inference
+    on 10000 held-out samples.  Prints one JSON line: training and inference throughput, held-out
+    accuracy, and the argmax agreement with the oracle given the same trained states."""
+    import torch
+    import oracle
+    from paper_2106_05373_amd import bcpnn, synth
+    from paper_2106_05373_amd.pipeline import Network
+
+    w = synth.WORKLOADS["mnist_pipeline"]
+    L = w.layer
+    B = w.batch
+    dev = torch.device("cuda", 0)
+    px, labels = synth.dataset(w)
+    tx, tlabels = synth.dataset(w, split="test")
+    X = synth.encode_pixels(px)
+    Xt = torch.from_numpy(synth.encode_pixels(tx)).to(dev)
+    onehot = synth.one_hot(labels, w.readout_mcu)
+    mask = synth.random_mask(L.in_hcu, L.out_hcu, synth.active_count(L.in_hcu, w.mask_frac),
+                             w.seed_mask)
+    cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
+                               gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
+                               seed=w.seed_noise)
+    net = Network(cfg, mask, w.readout_mcu)
+    per_epoch = (w.n_train + B - 1) // B
+
+    def epoch_data(e):
+        perm = synth.epoch_permutation(w.n_train, w.seed_shuffle, e)
+        return (torch.from_numpy(X[perm]).to(dev), torch.from_numpy(onehot[perm]).to(dev))
+
+    # hidden layer: unsupervised, structural plasticity before every period-th batch
+    t_hidden = 0.0
+    for e in range(w.epochs):
+        xe, _ = epoch_data(e)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(per_epoch):
+            if w.period > 0 and (k + 1) % w.period == 0:
+                net.hidden.structural_update(count=False)
+            net.train_hidden(xe[k * B:(k + 1) * B])
+        torch.cuda.synchronize()
+        t_hidden += time.perf_counter() - t0
+    # readout: supervised, hidden layer frozen
+    t_read = 0.0
+    for e in range(w.epochs, w.epochs + w.readout_epochs):
+        xe, te = epoch_data(e)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(per_epoch):
+            net.train_readout(xe[k * B:(k + 1) * B], te[k * B:(k + 1) * B])
+        torch.cuda.synchronize()
+        t_read += time.perf_counter() - t0
+    # held-out inference
+    pred = torch.empty(len(tlabels), device=dev, dtype=torch.int32)
+    for k in range(0, len(tlabels), B):                      # warm-up pass
+        net.predict(Xt[k:k + B], out=pred[k:k + B])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(0, len(tlabels), B):
+        net.predict(Xt[k:k + B], out=pred[k:k + B])
+    torch.cuda.synchronize()
+    t_inf = time.perf_counter() - t0
+    pred = pred.cpu().numpy()
+
+    # the oracle's inference from the same trained states
+    hs, rs = net.hidden.get_state(), net.readout.get_state()
+    ho = oracle.OracleLayer(oracle.make_params(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu,
+                                               gain=w.gain, bias_gain=w.bias_gain), hs["mask"])
+    ho.set_state(hs)
+    ro = oracle.OracleLayer(oracle.make_params(L.out_hcu, L.out_mcu, 1, w.readout_mcu), rs["mask"])
+    ro.set_state(rs)
+    t0 = time.perf_counter()
+    xt_host = Xt.cpu().numpy()
+    ora = np.concatenate([ro.readout(ho.forward(xt_host[k:k + 1000])[1])[:, 0]
+                          for k in range(0, len(tlabels), 1000)])
+    t_ora = time.perf_counter() - t0
+    n_train = per_epoch * B
+    out = {
+        "metric": "C2 pipeline: held-out inference samples/s (hidden forward + readout argmax)",
+        "value": round(len(tlabels) / t_inf, 1), "unit": "samples/s", "n_gpus": 1,
+        "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: hidden {L.in_hcu}x{L.in_mcu} -> {L.out_hcu}x{L.out_mcu} "
+                               f"for {w.epochs} epochs (alpha {w.alpha}, gain {w.gain}, k_B "
+                               f"{w.bias_gain}, plasticity every {w.period} batches), "
+                               f"readout {L.out_hcu}x{L.out_mcu} -> 1x{w.readout_mcu} for "
+                               f"{w.readout_epochs} epoch, {len(tlabels)} held-out samples",
+                   "global_batch": B},
+        "hidden_train_samples_per_s": round(w.epochs * w.n_train / t_hidden, 1),
+        "readout_train_samples_per_s": round(w.readout_epochs * w.n_train / t_read, 1),
+        "heldout_accuracy": round(float(np.mean(pred == tlabels)), 4),
+        "oracle_heldout_accuracy": round(float(np.mean(ora == tlabels)), 4),
+        "oracle_argmax_agreement": round(float(np.mean(pred == ora)), 6),
+        "oracle_inference_samples_per_s": round(len(tlabels) / t_ora, 1),
+        "oracle_cores": oracle.threads(),
+    }
+    print(json.dumps(out), flush=True)
+    net.close()
+
+
+def run_precision_report(args):
+    """One epoch of the MNIST-shaped layer with Pij and W stored in fp32, bf16 and a 10-bit
+    mantissa on the GPU, and the fp32 oracle beside them on the same batches (free runs).
+    Reports the trace and weight error of each against the oracle and the agreement of the
+    hidden code (winning MCU per hidden HCU) on held-out samples."""
+    import torch
+    import oracle
+    from paper_2106_05373_amd import bcpnn, synth
+
+    w = synth.WORKLOADS["mnist_pipeline"]            # settings under which a code forms
+    L = w.layer
+    B = w.batch
+    dev = torch.device("cuda", 0)
+    px, _ = synth.dataset(w)
+    tx, _ = synth.dataset(w, split="test", n=2000)
+    X = synth.encode_pixels(px)
+    Xt = synth.encode_pixels(tx)
+    perm = synth.epoch_permutation(w.n_train, w.seed_shuffle, 0)
+    Xe = X[perm]
+    mask = synth.random_mask(L.in_hcu, L.out_hcu, synth.active_count(L.in_hcu, w.mask_frac),
+                             w.seed_mask)
+    kw = dict(alpha=w.alpha, gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
+              seed=w.seed_noise)
+    layers = {st: bcpnn.Layer(bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B,
+                                                   storage=st, **kw), mask)
+              for st in ("f32", "bf16", "m10")}
+    ora = oracle.OracleLayer(oracle.make_params(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, **kw),
+                             mask)
+    Xd = torch.from_numpy(Xe).to(dev)
+    per_epoch = (w.n_train + B - 1) // B
+    t0 = time.perf_counter()
+    for k in range(per_epoch):
+        plastic = w.period > 0 and (k + 1) % w.period == 0
+        for lay in layers.values():
+            if plastic:
+                lay.structural_update(count=False)
+            lay.train_batch(Xd[k * B:(k + 1) * B])
+        if plastic:
+            ora.structural_update()
+        ora.train_batch(Xe[k * B:(k + 1) * B])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    def code(y):                                     # winning MCU of every hidden HCU
+        return y.reshape(len(y), L.out_hcu, L.out_mcu).argmax(-1)
+
+    so = ora.get_state()
+    code_o = code(ora.forward(Xt)[1])
+    report = {}
+    yt = torch.empty((B, L.out_hcu * L.out_mcu), device=dev, dtype=torch.float32)
+    xtd = torch.from_numpy(Xt).to(dev)
+    for st, lay in layers.items():
+        sg = lay.get_state()
+        ys = []
+        for k in range(0, len(Xt), B):
+            n = min(B, len(Xt) - k)
+            lay.forward(xtd[k:k + n], yt[:n])
+            ys.append(yt[:n].cpu().numpy())
+        code_g = code(np.concatenate(ys))
+        werr = np.abs(sg["w"].astype(np.float64) - so["w"]) / np.maximum(1.0, np.abs(so["w"]))
+        report[st] = {
+            "pij_max_abs_err": float(np.max(np.abs(sg["pij"] - so["pij"]))),
+            "pi_max_abs_err": float(np.max(np.abs(sg["pi"] - so["pi"]))),
+            "pj_max_abs_err": float(np.max(np.abs(sg["pj"] - so["pj"]))),
+            "w_max_scaled_err": float(werr.max()),
+            "mask_differs": int(np.sum(sg["mask"] != so["mask"])),
+            "hidden_code_agreement": round(float(np.mean(code_g == code_o)), 6),
+        }
+        lay.close()
+    out = {"metric": "reduced-precision storage against the fp32 oracle (free runs, one epoch)",
+           "config": {"workload": f"{w.name} hidden layer: {L.in_hcu}x{L.in_mcu} -> "
+                                  f"{L.out_hcu}x{L.out_mcu}, alpha {w.alpha}, gain {w.gain}, "
+                                  f"k_B {w.bias_gain}, plasticity every {w.period} batches, "
+                                  f"{per_epoch} batches of {B}; hidden code on {len(Xt)} "
+                                  f"held-out samples", "global_batch": B},
+           "data": "synthetic", "storage": report, "wall_s": round(elapsed, 1)}
+    print(json.dumps(out), flush=True)
+
+
+def run_inference_sweep(args):
+    """Forward-pass (support + softmax) throughput of the MNIST-shaped layer by batch size."""
+    import torch
+    from paper_2106_05373_amd import bcpnn, synth
+
+    w = synth.WORKLOADS["mnist"]
+    L = w.layer
+    sizes = [1, 8, 32, 128, 512, 2048, 8192]
+    dev = torch.device("cuda", 0)
+    px, _ = synth.dataset(w, n=max(sizes))
+    X = torch.from_numpy(synth.encode_pixels(px)).to(dev)
+    mask = synth.random_mask(L.in_hcu, L.out_hcu, synth.active_count(L.in_hcu, w.mask_frac),
+                             w.seed_mask)
+    stream = torch.cuda.Stream(device=dev)
+    layer = bcpnn.Layer(bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu,
+                                             max(sizes), alpha=w.alpha), mask, stream=stream)
+    Y = torch.empty((max(sizes), L.out_hcu * L.out_mcu), device=dev, dtype=torch.float32)
+    rows = []
+    for B in sizes:
+        reps = max(20, min(2000, 200000 // B))
+        for _ in range(10):
+            layer.forward(X[:B], Y[:B])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            layer.forward(X[:B], Y[:B])
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / reps
+        rows.append({"batch": B, "us_per_batch": round(dt * 1e6, 2),
+                     "samples_per_s": round(B / dt, 1)})
+    layer.close()
+    print(json.dumps({"metric": "inference samples/s by batch size (support + per-HCU softmax)",
+                      "config": {"workload": f"mnist layer {L.in_hcu}x{L.in_mcu} -> "
+                                             f"{L.out_hcu}x{L.out_mcu}, 10% receptive fields"},
+                      "data": "synthetic", "dtype": "f32 (fp64 accumulation)",
+                      "sweep": rows}), flush=True)
 
 
 def cpu_baseline(w, mask, shuffled, sched, budget_s):

@@ -61,6 +61,7 @@ class Workload:
     mask_frac: float          # fraction of input HCUs active per hidden HCU (1.0 = full)
     period: int               # structural-plasticity period in batches (0 = never)
     gain: float = 1.0
+    bias_gain: float = 1.0    # k_B of the hidden layer
     seed_data: int = 0
     seed_test: int = 1
     seed_mask: int = 2
@@ -88,9 +89,11 @@ WORKLOADS = {
                      seed_data=0, seed_test=0, seed_mask=0, seed_shuffle=0, seed_noise=0),
     # 28x28 strokes -> 30 x 100, 10% receptive fields, plasticity every 100 batches.
     "mnist": _mnist_like("mnist"),
-    # the same hidden layer trained for 3 epochs plus a 1 x 10 supervised readout.
+    # the same hidden layer trained for 3 epochs plus a 1 x 10 supervised readout.  Learning
+    # settings under which 3 epochs form a hidden code (alpha 1e-3 with k_B = 1 collapses every
+    # hidden HCU onto one winning MCU in that time).
     "mnist_pipeline": _mnist_like("mnist_pipeline", epochs=3, n_test=10000, readout_mcu=10,
-                                  readout_epochs=1),
+                                  readout_epochs=1, alpha=1e-2, gain=4.0, bias_gain=0.0),
     # 96x96x3 textures -> 100 x 100, 5% receptive fields, plasticity every 20 batches.
     "stl": Workload(name="stl", data="textures96", n_train=5000,
                     layer=LayerShape(27648, 2, 100, 100), batch=256, alpha=1e-3, epochs=1,
