@@ -60,6 +60,7 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr int kWaves = 4;           // waves (32 x 32 blocks) per workgroup, along the columns
 constexpr int kChunk = 4;           // k-steps (16 batch rows each) of operands per round trip
 constexpr int kSums = 8;            // column-sum tiles requested up front (the batch for B <= 128)
+constexpr int kSweepRows = 16;      // row blocks per sweep over the column groups (see below)
 constexpr uint32_t kDrop = 0x80000000u;   // byte offset past every block's buffer range
 
 // Buffer resource over [p, p + bytes): raw (stride 0) addressing, 32-bit data format.  A load
@@ -86,10 +87,18 @@ __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_e
 trace_kernel(Geometry g, TraceArgs a, int n_cg) {
     const int lane = threadIdx.x & 63;
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
-    // workgroup -> (row block, group of kWaves column blocks), XCD-major
+    // workgroup -> (row block, group of kWaves column blocks).  The workgroups of one XCD take
+    // one contiguous stretch of this order, which sweeps kSweepRows row blocks over every column
+    // group, column group by column group: the x fragments of the sweep (kSweepRows blocks) stay
+    // in the XCD's L2 while the t fragments stream through it once per sweep.
+    const int n_rb = (n_in + 31) / 32;
     const int wg = (int)xcd_linear_index(blockIdx.x, gridDim.x);
-    const int bi = wg / n_cg;
-    const int bj = (wg % n_cg) * kWaves + (threadIdx.x >> 6);
+    const int sweep = wg / (kSweepRows * n_cg);
+    const int in_sweep = wg % (kSweepRows * n_cg);
+    const int rows_here = n_rb - sweep * kSweepRows < kSweepRows ? n_rb - sweep * kSweepRows
+                                                                  : kSweepRows;
+    const int bi = sweep * kSweepRows + in_sweep % rows_here;
+    const int bj = (in_sweep / rows_here) * kWaves + (threadIdx.x >> 6);
     const int i0 = bi * 32, j0 = bj * 32;
     if (j0 >= n_out) return;                                   // wave-uniform; no barriers
     const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
