@@ -274,6 +274,8 @@ SHAPES = {
     "wide_300": (30, 2, 2, 300, 30, 16),          # four
     "wide_1024": (20, 2, 2, 1024, 7, 17),         # eight (the largest out_mcu)
     "single_hidden_mcu": (25, 2, 40, 1, 5, 20),
+    "batch_200": (40, 2, 4, 24, 20, 200),          # 13 row tiles: past the 8 summed up front
+    "batch_256_odd_mcus": (33, 3, 5, 7, 11, 256),  # M_out 7 (scalar weight rows), 16 k-steps
 }
 
 
