@@ -68,7 +68,9 @@ typedef struct {
     int32_t out_hcu, out_mcu;   /* hidden HCUs and MCUs per HCU (> 0, out_mcu <= 1024,
                                    N_out <= 2^22)                                            */
     int32_t max_batch;          /* largest B accepted by forward/train_batch/readout,
-                                   in [1, 2^20]                                              */
+                                   in [1, 2^20]; also N_in * N_out <= 2^35,
+                                   in_hcu * out_hcu <= 2^26, ceil(max_batch / 16) * out_hcu
+                                   <= 2^23 (launch grids stay below 2^32 work-items)          */
     float alpha;                /* trace rate l of Alg. 1, in (0, 1]; from a time constant
                                    tau (in batches) use alpha = 1 / tau                      */
     int32_t n_cycles;           /* repetitions of the trace/weight cycle per batch (>= 1);

@@ -83,6 +83,11 @@ const char* check_config(const bcpnn_config* c) {
     if ((n_in + 63) / 64 > 65535) return "N_in exceeds 65535 * 64";
     if (n_out > (1ll << 22)) return "N_out exceeds 2^22";      // a 64-row Pij tile < 2^30 bytes
     if (c->max_batch <= 0 || c->max_batch > (1 << 20)) return "max_batch must lie in [1, 2^20]";
+    // every launch grid stays below 2^32 work-items
+    if (n_in * n_out > (1ll << 35)) return "N_in * N_out exceeds 2^35";
+    if ((int64_t)c->in_hcu * c->out_hcu > (1ll << 26)) return "in_hcu * out_hcu exceeds 2^26";
+    if ((int64_t)((c->max_batch + 15) / 16) * c->out_hcu > (1ll << 23))
+        return "ceil(max_batch / 16) * out_hcu exceeds 2^23";
     if (!(c->alpha > 0.0f && c->alpha <= 1.0f)) return "alpha must lie in (0, 1]";
     if (c->n_cycles < 1) return "n_cycles must be >= 1";
     if (!(c->gain >= 0.0f) || !isfinite(c->gain)) return "gain must be finite and >= 0";

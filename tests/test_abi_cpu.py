@@ -57,6 +57,8 @@ BAD = {
     "max_batch 0": dict(max_batch=0),
     "max_batch above 2^20": dict(max_batch=(1 << 20) + 1),
     "N_out above 2^22": dict(out_hcu=(1 << 22) // 1024 + 1, out_mcu=1024),
+    "HCU pairs above 2^26": dict(in_hcu=40000, out_hcu=2000, out_mcu=1),
+    "row tiles x hidden HCUs above 2^23": dict(max_batch=1 << 20, out_hcu=200, out_mcu=1),
     "swaps negative": dict(n_swaps=-1),
     "swaps too many": dict(n_swaps=257),
     "storage unknown": dict(storage=7),
