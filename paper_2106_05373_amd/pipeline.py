@@ -25,13 +25,15 @@ class Network:
 
     def __init__(self, hidden_cfg: bcpnn.Config, hidden_mask: Optional[np.ndarray],
                  n_classes: int, readout_alpha: Optional[float] = None, stream=None):
+        """The readout takes the hidden layer's alpha (unless readout_alpha is given) and its
+        storage format, k_B = 1 and a full mask."""
         import torch
         self.torch = torch
         self.hidden = bcpnn.Layer(hidden_cfg, hidden_mask, stream=stream)
         rc = bcpnn.default_config(hidden_cfg.out_hcu, hidden_cfg.out_mcu, 1, n_classes,
                                   hidden_cfg.max_batch,
                                   alpha=hidden_cfg.alpha if readout_alpha is None else readout_alpha,
-                                  seed=hidden_cfg.seed + 1)
+                                  seed=hidden_cfg.seed + 1, storage=hidden_cfg.storage)
         self.readout = bcpnn.Layer(rc, None, stream=stream)
         self.n_classes = n_classes
         self.max_batch = hidden_cfg.max_batch
