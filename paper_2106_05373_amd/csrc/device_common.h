@@ -52,6 +52,46 @@ __device__ __forceinline__ int64_t xcd_linear_index(int64_t bid, int64_t total) 
     return xcd * q + (xcd < rem ? xcd : rem) + slot;
 }
 
+// Workgroup barrier that orders LDS only: the fences are limited to the local address space, so
+// the barrier waits for this wave's LDS operations (lgkmcnt) but leaves its global loads and
+// stores in flight (a plain __syncthreads also drains vmcnt).  For kernels whose waves exchange
+// data through LDS alone.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Wave-wide reductions over data-parallel-primitive lane moves (no LDS round trips): partial
+// results climb the lanes of each 16-lane row (shift right by 1, 2, 4, 8), then rows 0 / 2
+// feed rows 1 / 3 (broadcast of lane 15) and rows 0-1 feed rows 2-3 (broadcast of lane 31);
+// lane 63 ends with the total, which is then read back to every lane.  Lanes a move cannot
+// fill keep the identity (`idle`).
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_move(float v, float idle) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+        __builtin_bit_cast(int, idle), __builtin_bit_cast(int, v), kCtrl, kRowMask, 0xf, false));
+}
+
+template <typename Op>
+__device__ __forceinline__ float wave_reduce_dpp(float v, float idle, Op op) {
+    v = op(v, dpp_move<0x111, 0xf>(v, idle));   // row_shr:1
+    v = op(v, dpp_move<0x112, 0xf>(v, idle));   // row_shr:2
+    v = op(v, dpp_move<0x114, 0xf>(v, idle));   // row_shr:4
+    v = op(v, dpp_move<0x118, 0xf>(v, idle));   // row_shr:8
+    v = op(v, dpp_move<0x142, 0xa>(v, idle));   // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp_move<0x143, 0xc>(v, idle));   // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+__device__ __forceinline__ float wave_max_dpp(float v) {
+    return wave_reduce_dpp(v, -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+}
+
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+    return wave_reduce_dpp(v, 0.0f, [](float a, float b) { return a + b; });
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);

@@ -52,8 +52,6 @@ struct SupportLayout {
     bool fits;                     // every thread's share of a chunk fits its staging slots
 };
 
-constexpr int kSplitCols = 128;   // input columns transposed per pass of the operand writer
-
 // Writes the 16 batch entries of unit u in k-step ks (one row tile) as bf16 hi and lo parts
 // (hi = bf16(v), lo = bf16(v - hi), round to nearest even): two 16-byte fragment chunks each.
 __device__ __forceinline__ void write_split_column(const float (&v)[kRows], uint16_t* hi,
@@ -104,9 +102,12 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     const int32_t k_total = act_count[hj] * g.in_mcu;
     const int32_t* alist = act_list + (int64_t)hj * g.in_hcu;
     const int64_t col_base = (int64_t)hj * g.out_mcu;
-    for (int32_t k = tid; k < k_total; k += kThreads)
-        units[k] = alist[k / g.in_mcu] * g.in_mcu + k % g.in_mcu;
-    __syncthreads();
+    // The table is filled up to the largest K_h of the layer, so its loads do not wait for the
+    // count; entries past k_total are never used.
+    for (int32_t k = tid; k < lay.k_alloc; k += kThreads)
+        units[k] = (int32_t)((uint32_t)alist[k / g.in_mcu] * (uint32_t)g.in_mcu +
+                             (uint32_t)(k % g.in_mcu));
+    lds_barrier();
 
     // Weight rows: row group grp takes chunk rows grp, grp + 16, ...; its 32 lanes take the
     // vectors sub, sub + 32, ... of each row.  Input panel: row r = grp, units sub, sub + 32, ...
@@ -169,11 +170,54 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
         col_of[t] = (nt < lay.n_tiles ? nt : lay.n_tiles - 1) * 16 + (lane & 15);
     }
 
+
+    // The input columns [c0, c1) of this workgroup's share of the x operand (see the epilogue),
+    // in passes of 64 columns (lane = column): wave w takes passes 7 - w, 15 - w, ...  A pass
+    // reads each of the 16 rows with one coalesced load (clamped in bounds, zero past the batch
+    // or the range); the first pass is fetched before the softmax so that its latency hides.
+    const int64_t c0 = (int64_t)hj * g.n_in / g.out_hcu;
+    const int64_t c1 = (int64_t)(hj + 1) * g.n_in / g.out_hcu;
+    const int rows = B - row0 < kRows ? B - row0 : kRows;
+    const int rt = row0 / kRows;
+    const int n_pass = (int)((c1 - c0 + 63) / 64);
+    const int pass0 = kWaves - 1 - wave;
+    float xcol[kRows];
+    auto split_load = [&](int p) {
+        const int64_t i = c0 + (int64_t)p * 64 + lane;
+        const int64_t ic = i < c1 ? i : c1 - 1;
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            const int rr = r < rows ? row0 + r : row0;
+            xcol[r] = x[(int64_t)rr * g.n_in + ic];
+        }
+    };
+    auto split_store = [&](int p) {
+        const int64_t i = c0 + (int64_t)p * 64 + lane;
+        float sum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            xcol[r] = r < rows ? xcol[r] : 0.0f;
+            sum += xcol[r];
+        }
+        if (i < c1) {
+            write_split_column(xcol, ops.x_hi, ops.x_lo, i, rt, ops.n_ks);
+            ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
+        }
+    };
+
     if (k_total > 0) load_chunk(0);
+    // Bias of this wave's columns, fetched now so that its latency hides behind the contraction
+    // (after the first chunk's loads, which complete first).
+    float bias_r[kTilesPerWave];
+#pragma unroll
+    for (int t = 0; t < kTilesPerWave; ++t) {
+        const int c = col_of[t] < g.out_mcu ? col_of[t] : g.out_mcu - 1;
+        bias_r[t] = bias[col_base + c];
+    }
     for (int32_t k0 = 0; k0 < k_total; k0 += kc) {
-        __syncthreads();                          // the previous chunk has been consumed
+        lds_barrier();                          // the previous chunk has been consumed
         store_chunk();
-        __syncthreads();
+        lds_barrier();
         if (k0 + kc < k_total) load_chunk(k0 + kc);   // in flight during the MFMAs below
         // k-steps of 4 units (the rows beyond k_total hold zeros): groups of 8, then the rest
         const int rem = k_total - k0 < kc ? k_total - k0 : kc;
@@ -203,14 +247,14 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
         }
     }
 
-    __syncthreads();   // done with the panels; the support tile reuses their LDS
+    lds_barrier();   // done with the panels; the support tile reuses their LDS
 #pragma unroll
     for (int t = 0; t < kTilesPerWave; ++t) {
         const int nt = wave + t * kWaves;
         if (nt < lay.n_tiles) {
             const int c = nt * 16 + (lane & 15);
             if (c < g.out_mcu) {
-                const double bj = (double)bias[col_base + c];
+                const double bj = (double)bias_r[t];
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                 {
@@ -221,60 +265,79 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 
-    // Each wave takes rows wave and wave + 8 together (independent reduction chains).
+    if (has_ops && pass0 < n_pass) split_load(pass0);
+
+    // Each wave takes rows wave and wave + 8 together (independent reduction chains), one LDS
+    // read per element: lane l holds columns l, l + 64, ... of both rows in registers
+    // (M_out <= 128 kTilesPerWave, so 2 kTilesPerWave of them).
     static_assert(kRows == 2 * kWaves, "two softmax rows per wave");
     {
+        constexpr int kPer = 2 * kTilesPerWave;
         const int ra = wave, rb = wave + kWaves;
         const bool va = row0 + ra < B, vb = row0 + rb < B;
         float* sa = stile + ra * mpad;
         float* sb = stile + rb * mpad;
         const int64_t oa = (int64_t)(row0 + ra) * g.n_out + col_base;
         const int64_t ob = (int64_t)(row0 + rb) * g.n_out + col_base;
+        float ea[kPer], eb[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int m = lane + 64 * q;
+            ea[q] = m < g.out_mcu ? sa[m] : -INFINITY;
+            eb[q] = m < g.out_mcu ? sb[m] : -INFINITY;
+        }
         if (s) {
-            for (int m = lane; m < g.out_mcu; m += 64) {
-                if (va) s[oa + m] = sa[m];
-                if (vb) s[ob + m] = sb[m];
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int m = lane + 64 * q;
+                if (m < g.out_mcu) {
+                    if (va) s[oa + m] = ea[q];
+                    if (vb) s[ob + m] = eb[q];
+                }
             }
         }
         if (mode == 0) {
             float ma = -INFINITY, mb = -INFINITY;
-            for (int m = lane; m < g.out_mcu; m += 64) {
-                ma = fmaxf(ma, sa[m]);
-                mb = fmaxf(mb, sb[m]);
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                ma = fmaxf(ma, ea[q]);
+                mb = fmaxf(mb, eb[q]);
             }
-            for (int off = 32; off > 0; off >>= 1) {
-                ma = fmaxf(ma, __shfl_xor(ma, off, 64));
-                mb = fmaxf(mb, __shfl_xor(mb, off, 64));
-            }
+            ma = wave_max_dpp(ma);
+            mb = wave_max_dpp(mb);
             float da = 0.0f, db = 0.0f;
-            for (int m = lane; m < g.out_mcu; m += 64) {
-                const float ea = expf(gain * (sa[m] - ma));
-                const float eb = expf(gain * (sb[m] - mb));
-                sa[m] = ea;
-                sb[m] = eb;
-                da += ea;
-                db += eb;
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const bool in = lane + 64 * q < g.out_mcu;
+                ea[q] = in ? expf(gain * (ea[q] - ma)) : 0.0f;
+                eb[q] = in ? expf(gain * (eb[q] - mb)) : 0.0f;
+                da += ea[q];
+                db += eb[q];
             }
-            for (int off = 32; off > 0; off >>= 1) {
-                da += __shfl_xor(da, off, 64);
-                db += __shfl_xor(db, off, 64);
-            }
+            da = wave_sum_dpp(da);
+            db = wave_sum_dpp(db);
             const float ia = 1.0f / da, ib = 1.0f / db;
-            for (int m = lane; m < g.out_mcu; m += 64) {
-                const float ya = sa[m] * ia, yb = sb[m] * ib;
-                sa[m] = ya;                           // kept for the contraction operands
-                sb[m] = yb;
-                if (va) y[oa + m] = ya;
-                if (vb) y[ob + m] = yb;
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int m = lane + 64 * q;
+                if (m < g.out_mcu) {
+                    const float ya = ea[q] * ia, yb = eb[q] * ib;
+                    sa[m] = ya;                       // kept for the contraction operands
+                    sb[m] = yb;
+                    if (va) y[oa + m] = ya;
+                    if (vb) y[ob + m] = yb;
+                }
             }
         } else {
             float bva = -INFINITY, bvb = -INFINITY;
             int bia = 0x7fffffff, bib = 0x7fffffff;
-            for (int m = lane; m < g.out_mcu; m += 64) {
-                if (sa[m] > bva) { bva = sa[m]; bia = m; }
-                if (sb[m] > bvb) { bvb = sb[m]; bib = m; }
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int m = lane + 64 * q;
+                if (m < g.out_mcu && ea[q] > bva) { bva = ea[q]; bia = m; }
+                if (m < g.out_mcu && eb[q] > bvb) { bvb = eb[q]; bib = m; }
             }
             for (int off = 32; off > 0; off >>= 1) {
                 const float ova = __shfl_xor(bva, off, 64), ovb = __shfl_xor(bvb, off, 64);
@@ -294,9 +357,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     // k-step): the hidden HCU's columns of t (the activity above, or the target) and the input
     // columns [c0, c1) of x, each column split into bf16 hi / lo parts and written in fragment
     // order, plus the column sums over these rows.  Rows past B are written as zeros.
-    const int rows = B - row0 < kRows ? B - row0 : kRows;
-    const int rt = row0 / kRows;
-    __syncthreads();
+    lds_barrier();
     for (int m = tid; m < g.out_mcu; m += kThreads) {
         float v[kRows];
         float sum = 0.0f;
@@ -311,28 +372,9 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
         write_split_column(v, ops.t_hi, ops.t_lo, col, rt, ops.n_ks);
         ops.t_sum[(int64_t)rt * g.n_out + col] = sum;
     }
-    const int64_t c0 = (int64_t)hj * g.n_in / g.out_hcu;
-    const int64_t c1 = (int64_t)(hj + 1) * g.n_in / g.out_hcu;
-    float* xt = stile;                                           // [kRows][kSplitCols]
-    for (int64_t cb = c0; cb < c1; cb += kSplitCols) {
-        __syncthreads();
-        for (int e = tid; e < kRows * kSplitCols; e += kThreads) {
-            const int r = e / kSplitCols, cc = e % kSplitCols;
-            xt[e] = (r < rows && cb + cc < c1) ? x[(int64_t)(row0 + r) * g.n_in + cb + cc] : 0.0f;
-        }
-        __syncthreads();
-        for (int cc = tid; cc < kSplitCols && cb + cc < c1; cc += kThreads) {
-            float v[kRows];
-            float sum = 0.0f;
-#pragma unroll
-            for (int r = 0; r < kRows; ++r) {
-                v[r] = xt[r * kSplitCols + cc];
-                sum += v[r];
-            }
-            const int64_t i = cb + cc;
-            write_split_column(v, ops.x_hi, ops.x_lo, i, rt, ops.n_ks);
-            ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
-        }
+    for (int p = pass0; p < n_pass; p += kWaves) {
+        if (p != pass0) split_load(p);
+        split_store(p);
     }
 }
 
@@ -371,9 +413,7 @@ size_t lds_bytes(const SupportLayout& L) {
     const size_t table = (size_t)((L.k_alloc + 3) & ~3) * sizeof(int32_t);
     const size_t panels = (size_t)L.kc * L.mpad * sizeof(float) +
                           (size_t)kRows * L.xstride * sizeof(float);
-    size_t tile = (size_t)kRows * L.mpad * sizeof(float);
-    const size_t split = (size_t)kRows * kSplitCols * sizeof(float);
-    if (split > tile) tile = split;
+    const size_t tile = (size_t)kRows * L.mpad * sizeof(float);
     return table + (panels > tile ? panels : tile);
 }
 

@@ -126,14 +126,27 @@ trace_kernel(Geometry g, TraceArgs a, int n_cg) {
 #pragma unroll
     for (int q = 0; q < kSums; ++q) part[q] = sums[(q < nk ? q : nk - 1) * st + u];
     const float p_old = is_row ? a.pi_old[u] : a.pj_old[u];
-    // mask bytes of the lane's 16 elements: HCU of every row / column unit, spread by lane reads
+    // Mask of the lane's column over the block's 32 rows, one bit per row.  HCU of every row /
+    // column unit, spread by lane reads.  When the block's columns fall in at most two hidden
+    // HCUs (always for M_out >= 32), lane l reads the byte of row l % 32 and hidden HCU
+    // hc0 + l / 32, and one ballot gives both HCUs' row masks; otherwise every lane reads the
+    // bytes of its 16 elements.
     const int hu = is_row ? u / g.in_mcu : u / g.out_mcu;
     const int hj = __shfl(hu, 32 + jl, 64);
-    uint32_t act[16];
+    const int hc0 = __shfl(hu, 32, 64), hc1 = __shfl(hu, 63, 64);
+    uint32_t act_bits = 0;
+    if (hc1 - hc0 <= 1) {                                      // wave-uniform
+        const int hr = __shfl(hu, jl, 64);
+        const int hc = hc0 + (lane >> 5) < hc1 ? hc0 + (lane >> 5) : hc1;
+        const uint64_t bits = __ballot(a.mask[(int64_t)hr * g.out_hcu + hc] != 0);
+        act_bits = hj == hc0 ? (uint32_t)bits : (uint32_t)(bits >> 32);
+    } else {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int hi = __shfl(hu, il0 + 8 * (r >> 2) + (r & 3), 64);
-        act[r] = a.mask[(int64_t)hi * g.out_hcu + hj];
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const int hi = __shfl(hu, il, 64);
+            act_bits |= (a.mask[(int64_t)hi * g.out_hcu + hj] != 0 ? 1u : 0u) << il;
+        }
     }
 
     // ---- contraction: operands straight from the fragment-order arrays -----------------------
@@ -191,7 +204,7 @@ trace_kernel(Geometry g, TraceArgs a, int n_cg) {
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pn), rp, jok ? off : kDrop, 0, 0);
         const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(wv), rw,
-                                              jok && act[r] ? off : kDrop, 0, 0);
+                                              jok && ((act_bits >> il) & 1u) ? off : kDrop, 0, 0);
     }
 }
 
