@@ -19,6 +19,8 @@ namespace {
 constexpr int32_t kMaxOutMcu = 1024;     // softmax segment held in LDS by the support kernel
 constexpr int32_t kMaxInHcu = 49152;     // mask column held in LDS by the swap kernel
 constexpr int32_t kMaxSwaps = 256;
+// operand sets: one group filling, up to two being swept
+constexpr int kSets = 3 * bcpnn::kMaxSweepBatches;
 
 thread_local std::string g_error;
 
@@ -37,7 +39,8 @@ bcpnn_status fail(bcpnn_status st, const char* fmt, ...) {
 struct bcpnn_layer {
     bcpnn_config cfg;
     Geometry g;
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr;        // the caller's stream
+    hipStream_t side = nullptr;          // the layer's own stream for the silent-trace sweep
     int drop_bits = 0;
     int32_t max_active = 0;              // largest active count of a hidden HCU (swaps keep it)
     float* pi[2] = {nullptr, nullptr};   // the trace kernel reads one and writes the other
@@ -52,10 +55,24 @@ struct bcpnn_layer {
     int32_t* swap_count = nullptr;       // [out_hcu]
     double* mi = nullptr;                // [in_hcu][out_hcu]
     float* y_buf = nullptr;              // [max_batch][n_out] activity when the caller gives none
-    bcpnn::TraceOperands ops{};          // split batch operands of the joint-trace contraction
+    // Split batch operands of the joint-trace contraction, kSets sets used in turn.  The silent
+    // elements of Pij take the updates of up to kMaxSweepBatches consecutive batches in one
+    // sweep on the side stream, which reads those batches' sets while later batches proceed.
+    bcpnn::TraceOperands ops[kSets] = {};
+    int ops_cur = 0;
+    int64_t set_sweep[kSets];            // sweep (sequence number) that frees the set, or -1
+    struct Pending { int set; int32_t B; float c1, c2; };
+    Pending pend[bcpnn::kMaxSweepBatches];
+    int n_pend = 0;                      // batches whose silent updates are not yet enqueued
+    hipEvent_t sweep_ready = nullptr;    // the pending batches' operands are written
+    hipEvent_t sweep_done[kSets] = {};   // ring of sweep completion events
+    int64_t n_sweeps = 0;                // sweeps enqueued; sweep k records sweep_done[k % kSets]
+    int64_t waited = -1;                 // the caller's stream already waits for sweeps <= this
+    bool full_mask = false;              // no silent block: no sweeps
+    int64_t sweep_wgs = 0;               // resident workgroups of a sweep (one per CU)
     bool mi_valid = false;
     bool failed = false;
-    int32_t profile_every = 0;           // 0: off; n: every n-th trace launch carries events
+    int32_t profile_every = 0;           // 0: off; n: every n-th sweep launch carries events
     int64_t trace_launches = 0;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
     size_t events_used = 0;
@@ -123,22 +140,97 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
     }
     if ((int64_t)max_active * c.in_mcu > bcpnn::kMaxActiveUnits)
         return "a hidden HCU has more than 12288 active input units (active HCUs * in_mcu)";
+    const Geometry g{c.in_hcu, c.in_mcu, c.out_hcu, c.out_mcu, (int64_t)c.in_hcu * c.in_mcu,
+                     (int64_t)c.out_hcu * c.out_mcu};
+    if (bcpnn::trace_active_workgroups(g, max_active) >= (1ll << 24))
+        return "the active-block trace launch would exceed 2^24 workgroups "
+               "(out_hcu * ceil(active units / 32) * ceil(out_mcu / 128) too large)";
     return nullptr;
 }
 
 void free_layer(bcpnn_layer* L) {
     if (!L) return;
     void* bufs[] = {L->pi[0], L->pi[1], L->pj[0], L->pj[1], L->pij, L->w, L->b, L->mask,
-                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf,
-                    L->ops.x_hi, L->ops.x_lo, L->ops.t_hi, L->ops.t_lo, L->ops.x_sum,
-                    L->ops.t_sum};
+                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
+    for (int k = 0; k < kSets; ++k) {
+        void* ob[] = {L->ops[k].x_hi, L->ops[k].x_lo, L->ops[k].t_hi, L->ops[k].t_lo,
+                      L->ops[k].x_sum, L->ops[k].t_sum};
+        for (void* p : ob)
+            if (p) (void)hipFree(p);
+        if (L->sweep_done[k]) (void)hipEventDestroy(L->sweep_done[k]);
+    }
+    if (L->sweep_ready) (void)hipEventDestroy(L->sweep_ready);
+    if (L->side) (void)hipStreamDestroy(L->side);
     for (auto& ev : L->events) {
         (void)hipEventDestroy(ev.first);
         (void)hipEventDestroy(ev.second);
     }
     delete L;
+}
+
+// Enqueues the silent-element sweep of the pending batches on the side stream, after the
+// caller's stream has written their operands.
+hipError_t launch_pending_sweep(bcpnn_layer* L) {
+    if (L->n_pend == 0) return hipSuccess;
+    bcpnn::SweepArgs a{};
+    for (int t = 0; t < L->n_pend; ++t) {
+        const bcpnn::TraceOperands& o = L->ops[L->pend[t].set];
+        a.bt[t] = bcpnn::SweepBatch{o.x_hi, o.x_lo, o.t_hi, o.t_lo,
+                                    (L->pend[t].B + 15) / 16, L->pend[t].c1, L->pend[t].c2};
+    }
+    a.n_batches = L->n_pend;
+    a.n_ks = L->ops[0].n_ks;
+    a.pij = L->pij;
+    a.mask = L->mask;
+    a.drop_bits = L->drop_bits;
+    std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
+    hipError_t e = hipSuccess;
+    if (L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
+        if (L->events_used == L->events.size()) {
+            std::pair<hipEvent_t, hipEvent_t> p{nullptr, nullptr};
+            e = hipEventCreate(&p.first);
+            if (e == hipSuccess) e = hipEventCreate(&p.second);
+            if (e != hipSuccess) return e;
+            L->events.push_back(p);
+        }
+        ev = &L->events[L->events_used++];
+    }
+    const int64_t seq = L->n_sweeps++;
+    const int slot = (int)(seq % kSets);
+    e = hipEventRecord(L->sweep_ready, L->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->sweep_ready, 0);
+    if (e == hipSuccess)
+        e = bcpnn::launch_trace_sweep(L->side, L->g, a, L->sweep_wgs, ev ? ev->first : nullptr,
+                                      ev ? ev->second : nullptr);
+    if (e == hipSuccess) e = hipEventRecord(L->sweep_done[slot], L->side);
+    if (e != hipSuccess) return e;
+    for (int t = 0; t < L->n_pend; ++t) L->set_sweep[L->pend[t].set] = seq;
+    L->n_pend = 0;
+    return hipSuccess;
+}
+
+// Makes the caller's stream wait for sweep seq and every earlier one (they run in order).
+hipError_t wait_sweep(bcpnn_layer* L, int64_t seq) {
+    if (seq <= L->waited) return hipSuccess;
+    const hipError_t e = hipStreamWaitEvent(L->stream, L->sweep_done[seq % kSets], 0);
+    if (e == hipSuccess) L->waited = seq;
+    return e;
+}
+
+// Applies the pending silent updates and makes the caller's stream wait for the last sweep:
+// every Pij is then current in stream order.
+hipError_t join_side(bcpnn_layer* L) {
+    hipError_t e = launch_pending_sweep(L);
+    if (e == hipSuccess && L->n_sweeps > 0) e = wait_sweep(L, L->n_sweeps - 1);
+    return e;
+}
+
+bool mask_is_full(const bcpnn_config& c, const std::vector<int32_t>& count) {
+    for (int32_t v : count)
+        if (v != c.in_hcu) return false;
+    return true;
 }
 
 bcpnn_status usable(const bcpnn_layer* L) {
@@ -201,6 +293,7 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
 
     bcpnn_layer* L = new bcpnn_layer();
     L->max_active = max_active;
+    L->full_mask = mask_is_full(*cfg, count);
     L->cfg = *cfg;
     L->g = Geometry{cfg->in_hcu, cfg->in_mcu, cfg->out_hcu, cfg->out_mcu,
                     (int64_t)cfg->in_hcu * cfg->in_mcu, (int64_t)cfg->out_hcu * cfg->out_mcu};
@@ -226,20 +319,36 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = dalloc(&L->y_buf, (size_t)cfg->max_batch * g.n_out);
     // split operands in fragment order: 1 KiB per 32 units and 16 batch rows; the units past
     // the layer in the last block are never written and must read as zero
-    L->ops.n_ks = (cfg->max_batch + 15) / 16;
-    const size_t n_rt = (size_t)L->ops.n_ks;
+    const int32_t n_ks = (cfg->max_batch + 15) / 16;
+    const size_t n_rt = (size_t)n_ks;
     const size_t xf = (size_t)((g.n_in + 31) / 32) * n_rt * 512;
     const size_t tf = (size_t)((g.n_out + 31) / 32) * n_rt * 512;
-    if (e == hipSuccess) e = dalloc(&L->ops.x_hi, xf);
-    if (e == hipSuccess) e = dalloc(&L->ops.x_lo, xf);
-    if (e == hipSuccess) e = dalloc(&L->ops.t_hi, tf);
-    if (e == hipSuccess) e = dalloc(&L->ops.t_lo, tf);
-    if (e == hipSuccess) e = dalloc(&L->ops.x_sum, n_rt * g.n_in);
-    if (e == hipSuccess) e = dalloc(&L->ops.t_sum, n_rt * g.n_out);
-    if (e == hipSuccess) e = hipMemsetAsync(L->ops.x_hi, 0, xf * sizeof(uint16_t), L->stream);
-    if (e == hipSuccess) e = hipMemsetAsync(L->ops.x_lo, 0, xf * sizeof(uint16_t), L->stream);
-    if (e == hipSuccess) e = hipMemsetAsync(L->ops.t_hi, 0, tf * sizeof(uint16_t), L->stream);
-    if (e == hipSuccess) e = hipMemsetAsync(L->ops.t_lo, 0, tf * sizeof(uint16_t), L->stream);
+    for (int k = 0; k < kSets; ++k) {
+        bcpnn::TraceOperands& o = L->ops[k];
+        o.n_ks = n_ks;
+        if (e == hipSuccess) e = dalloc(&o.x_hi, xf);
+        if (e == hipSuccess) e = dalloc(&o.x_lo, xf);
+        if (e == hipSuccess) e = dalloc(&o.t_hi, tf);
+        if (e == hipSuccess) e = dalloc(&o.t_lo, tf);
+        if (e == hipSuccess) e = dalloc(&o.x_sum, n_rt * g.n_in);
+        if (e == hipSuccess) e = dalloc(&o.t_sum, n_rt * g.n_out);
+        if (e == hipSuccess) e = hipMemsetAsync(o.x_hi, 0, xf * sizeof(uint16_t), L->stream);
+        if (e == hipSuccess) e = hipMemsetAsync(o.x_lo, 0, xf * sizeof(uint16_t), L->stream);
+        if (e == hipSuccess) e = hipMemsetAsync(o.t_hi, 0, tf * sizeof(uint16_t), L->stream);
+        if (e == hipSuccess) e = hipMemsetAsync(o.t_lo, 0, tf * sizeof(uint16_t), L->stream);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&L->sweep_done[k], hipEventDisableTiming);
+        L->set_sweep[k] = -1;
+    }
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->sweep_ready, hipEventDisableTiming);
+    // default priority; non-blocking, so that it never waits for a legacy default stream
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
+    // The sweep keeps one workgroup (one wave per SIMD) resident per CU, which leaves room on
+    // every CU for the support and active-block workgroups of the batches it overlaps.
+    int dev = 0, n_cu = 0;
+    if (e == hipSuccess) e = hipGetDevice(&dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) L->sweep_wgs = n_cu;
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,
@@ -282,7 +391,9 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
 
 void bcpnn_layer_destroy(bcpnn_layer* L) {
     if (!L) return;
+    if (!L->failed) (void)join_side(L);
     (void)hipStreamSynchronize(L->stream);
+    if (L->side) (void)hipStreamSynchronize(L->side);
     free_layer(L);
 }
 
@@ -307,12 +418,16 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
         return fail(BCPNN_EINVAL, "device buffers must be 16-byte aligned");
     if (bcpnn_status st = check_batch(L, B)) return st;
     float* y = y_dev ? y_dev : L->y_buf;
+    const int set = L->ops_cur;
+    // the operand set is free once the sweep that read it last has run
+    if (L->set_sweep[set] >= 0) HIP_TRY(L, wait_sweep(L, L->set_sweep[set]));
+    L->set_sweep[set] = -1;
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 0, y, nullptr,
-                                     nullptr, target_dev, &L->ops));
+                                     nullptr, target_dev, &L->ops[set]));
     const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
     bcpnn::TraceArgs a;
-    a.ops = L->ops;
+    a.ops = L->ops[set];
     a.B = B;
     a.a_eff = (float)a_eff;
     a.c1 = (float)(1.0 - a_eff);
@@ -330,7 +445,7 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     a.bias_gain = L->cfg.bias_gain;
     a.drop_bits = L->drop_bits;
     std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
-    if (L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
+    if (L->full_mask && L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
         if (L->events_used == L->events.size()) {
             std::pair<hipEvent_t, hipEvent_t> p;
             HIP_TRY(L, hipEventCreate(&p.first));
@@ -339,14 +454,24 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
         }
         ev = &L->events[L->events_used++];
     }
-    HIP_TRY(L, bcpnn::launch_trace_update(L->stream, L->g, a, ev ? ev->first : nullptr,
+    if (!L->full_mask) {
+        // The silent elements: swept once per kMaxSweepBatches batches on the side stream,
+        // which needs only the operands (written above) and touches no element the active
+        // kernel below writes.
+        L->pend[L->n_pend++] = bcpnn_layer::Pending{set, B, a.c1, a.c2};
+        if (L->n_pend == bcpnn::kMaxSweepBatches) HIP_TRY(L, launch_pending_sweep(L));
+    }
+    HIP_TRY(L, bcpnn::launch_trace_active(L->stream, L->g, a, L->act_list, L->act_count,
+                                          L->max_active, ev ? ev->first : nullptr,
                                           ev ? ev->second : nullptr));
     L->cur = 1 - L->cur;
+    L->ops_cur = (set + 1) % kSets;
     return BCPNN_OK;
 }
 
 bcpnn_status bcpnn_recompute_weights(bcpnn_layer* L) {
     if (bcpnn_status st = usable(L)) return st;
+    HIP_TRY(L, join_side(L));
     HIP_TRY(L, bcpnn::launch_recompute_weights(L->stream, L->g, L->mask, L->pi[L->cur],
                                                L->pj[L->cur], L->pij, L->cfg.eps,
                                                L->cfg.bias_gain, L->drop_bits, L->w, L->b));
@@ -355,6 +480,7 @@ bcpnn_status bcpnn_recompute_weights(bcpnn_layer* L) {
 
 bcpnn_status bcpnn_structural_update(bcpnn_layer* L, int32_t* n_swapped_host) {
     if (bcpnn_status st = usable(L)) return st;
+    HIP_TRY(L, join_side(L));
     HIP_TRY(L, bcpnn::launch_mutual_information(L->stream, L->g, L->pi[L->cur], L->pj[L->cur],
                                                 L->pij, L->cfg.eps, L->mi));
     L->mi_valid = true;
@@ -398,6 +524,7 @@ bcpnn_status bcpnn_get_state(const bcpnn_layer* Lc, const bcpnn_state_view* v) {
     auto d2h = [&](void* dst, const void* src, size_t bytes) {
         return dst ? hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, L->stream) : hipSuccess;
     };
+    HIP_TRY(L, join_side(L));
     HIP_TRY(L, d2h(v->pi, L->pi[L->cur], (size_t)g.n_in * sizeof(float)));
     HIP_TRY(L, d2h(v->pj, L->pj[L->cur], (size_t)g.n_out * sizeof(float)));
     HIP_TRY(L, d2h(v->pij, L->pij, E * sizeof(float)));
@@ -419,6 +546,7 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     const Geometry& g = L->g;
     const size_t E = (size_t)g.n_in * (size_t)g.n_out;
     const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
+    HIP_TRY(L, join_side(L));
     HIP_TRY(L, hipMemcpyAsync(L->pi[L->cur], v->pi, (size_t)g.n_in * sizeof(float),
                               hipMemcpyHostToDevice, L->stream));
     HIP_TRY(L, hipMemcpyAsync(L->pj[L->cur], v->pj, (size_t)g.n_out * sizeof(float),
@@ -435,6 +563,7 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     HIP_TRY(L, bcpnn::launch_apply_mask(L->stream, g, L->mask, L->w));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
     L->max_active = max_active;
+    L->full_mask = mask_is_full(L->cfg, count);
     L->mi_valid = false;
     return BCPNN_OK;
 }
@@ -461,6 +590,7 @@ bcpnn_status bcpnn_profile_enable(bcpnn_layer* L, int32_t enable) {
 bcpnn_status bcpnn_profile_read(bcpnn_layer* L, double* total_ms, int32_t* launches) {
     if (bcpnn_status st = usable(L)) return st;
     if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
+    HIP_TRY(L, join_side(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
     double sum = 0.0;
     for (size_t k = 0; k < L->events_used; ++k) {

@@ -77,7 +77,8 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
 // support kernel keeps in its LDS unit table.
 constexpr int32_t kMaxActiveUnits = 12288;
 
-// Joint-trace contraction with the fused trace, weight and bias updates:
+// Joint-trace contraction with the trace, weight and bias updates, in two kernels that touch
+// disjoint elements of Pij:
 //   Pij <- c1 Pij + c2 sum_b x[b,i] t[b,j];  Pi, Pj from the batch means (read *_old, write
 //   *_new); w on active blocks; b = bias_gain log(max(Pj_new, eps)).  The batch enters as the
 //   split operands and column sums written by the support kernel.
@@ -96,9 +97,40 @@ struct TraceArgs {
     float eps, bias_gain;
     int drop_bits;
 };
-// start / stop (nullable) receive the kernel's own start and end time stamps.
-hipError_t launch_trace_update(hipStream_t stream, const Geometry& g, const TraceArgs& a,
-                               hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
+// The elements of active blocks (the rows of each hidden HCU's active input units), their
+// weights, and Pi, Pj, b of every unit.  max_active as for launch_support.
+hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const TraceArgs& a,
+                               const int32_t* act_list, const int32_t* act_count,
+                               int32_t max_active, hipEvent_t start = nullptr,
+                               hipEvent_t stop = nullptr);
+// Workgroups of that launch (for the launch-size check).
+int64_t trace_active_workgroups(const Geometry& g, int32_t max_active);
+// The elements of silent blocks over several consecutive batches: each element is read once,
+// takes the batches' updates Pij <- c1 Pij + c2 T in order (rounded to the storage format after
+// each, exactly as per-batch updates), and is written once.  Reads the mask; Pi, Pj, w and b
+// are untouched.  start / stop (nullable) receive the kernel's own start and end time stamps.
+constexpr int kMaxSweepBatches = 4;
+struct SweepBatch {
+    const uint16_t* x_hi;
+    const uint16_t* x_lo;
+    const uint16_t* t_hi;
+    const uint16_t* t_lo;
+    int32_t nk;       // k-steps of this batch: ceil(B / 16)
+    float c1, c2;     // 1 - a_eff and a_eff / B
+};
+struct SweepArgs {
+    SweepBatch bt[kMaxSweepBatches];
+    int32_t n_batches;
+    int32_t n_ks;     // k-steps per unit block of the operand arrays
+    float* pij;
+    const uint8_t* mask;
+    int drop_bits;
+};
+// resident_wgs > 0 caps the grid at that many workgroups (rounded up to a multiple of 8), each
+// looping over the 32 x 128 block groups; 0 launches one workgroup per group.
+hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const SweepArgs& a,
+                              int64_t resident_wgs, hipEvent_t start = nullptr,
+                              hipEvent_t stop = nullptr);
 
 // Mutual information of every (input HCU, hidden HCU) block, fp64, [in_hcu][out_hcu].
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,

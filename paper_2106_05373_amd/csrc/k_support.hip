@@ -23,6 +23,8 @@
 //
 // MFMA f64 16x16x4 lane layout (verified on gfx950): A[i][k] from lane i + 16 k, B[k][j] from
 // lane j + 16 k, and lane l holds D[l / 16 + 4 r][l % 16] in result register r.
+#include <mutex>
+
 #include "bcpnn_internal.h"
 #include "device_common.h"
 
@@ -379,6 +381,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
 }
 
 constexpr size_t kLdsBudget = 120 * 1024;
+constexpr size_t kLdsLimit = 160 * 1024;   // LDS of one gfx950 workgroup
 
 SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) {
     SupportLayout L;
@@ -430,13 +433,22 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     const size_t lds = lds_bytes(lay);
     const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
     const int64_t blocks = (int64_t)lay.n_row_tiles * g.out_hcu;
+    // allow dynamic LDS beyond 64 KB (gfx950 has 160 KB per workgroup): raised once, for every
+    // variant, to the largest size a launch can ask for
+    static std::once_flag raised;
+    std::call_once(raised, [] {
+        const void* all[] = {(const void*)support_kernel<1, 4>, (const void*)support_kernel<2, 4>,
+                             (const void*)support_kernel<4, 4>,
+                             (const void*)support_kernel<kMaxTilesPerWave, 4>,
+                             (const void*)support_kernel<1, 1>, (const void*)support_kernel<2, 1>,
+                             (const void*)support_kernel<4, 1>,
+                             (const void*)support_kernel<kMaxTilesPerWave, 1>};
+        for (const void* k : all)
+            (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      (int)kLdsLimit);
+        (void)hipGetLastError();
+    });
     auto go = [&](auto kernel) {
-        if (lds > 64 * 1024) {
-            // allow dynamic LDS beyond 64 KB (gfx950 has 160 KB per workgroup)
-            (void)hipFuncSetAttribute((const void*)kernel,
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            (void)hipGetLastError();
-        }
         const TraceOperands o = ops ? *ops : TraceOperands{};
         kernel<<<(unsigned)blocks, kThreads, lds, stream>>>(g, lay, x, B, w, bias, act_list,
                                                             act_count, gain, mode, y, s, winner,

@@ -1,8 +1,8 @@
-// Joint-trace contraction with the fused trace, weight and bias updates (Alg. 1 cycle loop):
+// Joint-trace contraction with the trace, weight and bias updates (Alg. 1 cycle loop):
 //
 //   T[i][j]  = sum_b x[b][i] t[b][j]                       (the batch sum of a_i (x) a_j)
 //   Pij     <- c1 Pij + c2 T[i][j]                         c1 = 1 - a_eff, c2 = a_eff / B
-//   Pi, Pj  <- c1 P + a_eff mean_b(.)                      (redundantly per block, see below)
+//   Pi, Pj  <- c1 P + a_eff mean_b(.)
 //   w[i][j]  = log max(Pij,eps) - log max(Pi,eps) - log max(Pj,eps)   on active blocks only
 //   b[j]     = k_B log max(Pj, eps)
 //
@@ -12,34 +12,41 @@
 // Design (gfx950):
 //  * T is a dense [N_in x N_out] product with K = B (the batch).  Every Pij is needed (silent
 //    connections are scored for plasticity), so the contraction is dense.
+//  * The update is split by the mask into two kernels that touch disjoint elements:
+//      - the active kernel updates the elements of active blocks (the rows of each hidden
+//        HCU's active input units, gathered) together with their weights, and the marginal
+//        traces and bias of every unit: everything the next batch's support reads;
+//      - the silent kernel sweeps the whole matrix and stores the elements of silent blocks.
+//    The library runs the silent kernel on a second stream, where it overlaps the next batch's
+//    support kernel (which never reads silent elements); every state access waits for it.
 //  * T runs on the bf16 matrix cores with a two-term split of both operands: v = hi + lo with
 //    hi = bf16(v), lo = bf16(v - hi), and T ~ lo.hi' + hi.lo' + hi.hi' (three
 //    v_mfma_f32_32x32x16_bf16, fp32 accumulation).  Each product is then exact to about 3
 //    parts in 2^17 (the dropped lo.lo' term and the rounding of lo), so T carries a relative
 //    error of order 1e-5; the trace update scales it by a_eff / B, which puts it near 1e-8 in
-//    Pij.  Three bf16 MFMAs cost 3/16 of the fp32 MFMA time of the same product, so the kernel
-//    is bound by memory: 8 bytes of Pij per element plus 4 per active weight from HBM, and the
-//    operands from L2.
+//    Pij.  Three bf16 MFMAs cost 3/16 of the fp32 MFMA time of the same product, so the
+//    kernels are bound by memory: 8 bytes of Pij per element plus 4 per active weight from
+//    HBM, and the operands from L2.
 //  * The support kernel of the same batch has already written x^T and t^T split, in MFMA
 //    fragment order (one 1 KiB chunk per 32 units and 16 batch rows), and the column sums of x
 //    and t per 16-row tile.
-//  * Every wave owns one 32 x 32 block of Pij and works alone: no LDS staging, no barrier.  It
-//    requests its Pij values, the inputs of its rows' and columns' marginal traces and its mask
-//    bytes first, then streams the operands straight into registers (each k-step of each
-//    operand is one contiguous 1 KiB read), four k-steps at a time, and runs the MFMAs.  The
-//    many independent waves in flight hide the memory latency; measured per wave, a block is
-//    two operand round trips plus the epilogue.
-//  * A workgroup is four waves on one row block and four neighbouring column blocks: they read
-//    the same x fragments (L1 hits after the first) and write 512 contiguous bytes of each row.
-//    Workgroups are ordered so that those of one XCD cover one contiguous stretch of blocks.
-//  * The marginal traces of the block's 32 rows (lanes 0..31) and 32 columns (lanes 32..63) are
-//    computed by the wave itself from the column sums (same code and order in every block,
-//    hence identical values) and spread to the lanes that need them with cross-lane reads; the
-//    blocks of the first block column / row store the new Pi / Pj and b.  Pi and Pj are read
-//    from one buffer and written to another (the host alternates them).
-//  * Pij values are buffer loads over the block's rows (rows past the layer read as zero); all
-//    stores are unconditional buffer stores, a store that must not happen getting an offset
-//    past the buffer range, which the hardware drops.  w is written on active blocks only.
+//  * Every wave owns one 32 x 32 block and works alone: no LDS staging, no barrier.  It
+//    requests its Pij values (and, in the active kernel, the inputs of its rows' and columns'
+//    marginal traces) first, then streams the operands straight into registers (each k-step of
+//    each operand is one contiguous 1 KiB read in the sweep, 32 16-byte pieces when the rows
+//    are gathered), four k-steps at a time, and runs the MFMAs.  The many independent waves in
+//    flight hide the memory latency.
+//  * Sweep: a workgroup is four waves on one row block and four neighbouring column blocks:
+//    they read the same x fragments (L1 hits after the first) and write 512 contiguous bytes
+//    of each row.  Workgroups are ordered so that those of one XCD cover one contiguous
+//    stretch of blocks.  Pij values are buffer loads over the block's rows (rows past the
+//    layer read as zero); all stores are unconditional buffer stores, a store that must not
+//    happen (an element of an active block, a column past the layer) getting an offset past
+//    the buffer range, which the hardware drops.
+//  * Marginals: Pi of a row and Pj of a column are computed from the column sums by the same
+//    code wherever they are needed (hence identical values); dedicated workgroups of the
+//    active kernel store Pi, Pj and b for every unit.  Pi and Pj are read from one buffer and
+//    written to another (the host alternates them).
 //
 // MFMA 32x32x16 bf16 lane layout (verified on gfx950): A[i][k] for k = 8 (l / 32) + 0..7 from
 // lane l = i + 32 (k / 8), B[k][j] likewise with j = l % 32, and lane l holds
@@ -59,6 +66,8 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int kWaves = 4;           // waves (32 x 32 blocks) per workgroup, along the columns
 constexpr int kChunk = 4;           // k-steps (16 batch rows each) of operands per round trip
+constexpr int kActiveChunk = 8;     // the same in the active kernel (few waves: one round trip
+                                    // covers a batch of 128)
 constexpr int kSums = 8;            // column-sum tiles requested up front (the batch for B <= 128)
 constexpr int kSweepRows = 16;      // row blocks per sweep over the column groups (see below)
 constexpr uint32_t kDrop = 0x80000000u;   // byte offset past every block's buffer range
@@ -82,89 +91,221 @@ __device__ __forceinline__ float to_storage(float v) {
     }
 }
 
+// Inputs of one unit's marginal trace: its column sums over the batch's 16-row tiles (the
+// first kSums requested up front) and its previous value.
+struct MarginalIn {
+    float part[kSums];
+    float p_old;
+};
+
+__device__ __forceinline__ void marginal_request(MarginalIn& m, const float* sums, int64_t st,
+                                                 int u, int nk, const float* p_old) {
+#pragma unroll
+    for (int q = 0; q < kSums; ++q) m.part[q] = sums[(q < nk ? q : nk - 1) * st + u];
+    m.p_old = p_old[u];
+}
+
+// P = c1 P_old + a_eff * (column sum / B); the same operations in the same order everywhere.
+__device__ __forceinline__ float marginal_value(const MarginalIn& m, const float* sums, int64_t st,
+                                                int u, int nk, const TraceArgs& a) {
+    float colsum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kSums; ++q)
+        if (q < nk) colsum += m.part[q];
+    for (int q = kSums; q < nk; ++q) colsum += sums[q * st + u];     // batches above 128
+    return fmaf(a.a_eff, colsum * a.inv_b, a.c1 * m.p_old);
+}
+
+// Silent sweep: every 32 x 32 block of Pij, updated by the contractions of a.n_batches
+// consecutive batches in order, storing the elements whose block is silent.
 template <int kDropBits>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3, 3)))
-trace_kernel(Geometry g, TraceArgs a, int n_cg) {
+trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work) {
     const int lane = threadIdx.x & 63;
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
-    // workgroup -> (row block, group of kWaves column blocks).  The workgroups of one XCD take
-    // one contiguous stretch of this order, which sweeps kSweepRows row blocks over every column
-    // group, column group by column group: the x fragments of the sweep (kSweepRows blocks) stay
-    // in the XCD's L2 while the t fragments stream through it once per sweep.
-    const int n_rb = (n_in + 31) / 32;
-    const int wg = (int)xcd_linear_index(blockIdx.x, gridDim.x);
-    const int sweep = wg / (kSweepRows * n_cg);
-    const int in_sweep = wg % (kSweepRows * n_cg);
-    const int rows_here = n_rb - sweep * kSweepRows < kSweepRows ? n_rb - sweep * kSweepRows
-                                                                  : kSweepRows;
-    const int bi = sweep * kSweepRows + in_sweep % rows_here;
-    const int bj = (in_sweep / rows_here) * kWaves + (threadIdx.x >> 6);
-    const int i0 = bi * 32, j0 = bj * 32;
-    if (j0 >= n_out) return;                                   // wave-uniform; no barriers
-    const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
-    const int cols = n_out - j0 < 32 ? n_out - j0 : 32;
-    const int nk = (a.B + 15) / 16;                            // k-steps = 16-row tiles
-    const int n_ks = a.ops.n_ks;
-    const int jl = lane & 31;
-    const int il0 = 4 * (lane >> 5);
+    // Persistent: workgroup b takes work items b, b + G, ... (G = gridDim.x, a multiple of 8, so
+    // they all lie on the workgroup's XCD).
+    for (int item = blockIdx.x; item < n_work; item += gridDim.x) {
+        // work item -> (row block, group of kWaves column blocks).  The items of one XCD form
+        // one contiguous stretch of this order, which sweeps kSweepRows row blocks over every
+        // column group, column group by column group: the x fragments of the sweep (kSweepRows
+        // blocks) stay in the XCD's L2 while the t fragments stream through it once per sweep.
+        const int n_rb = (n_in + 31) / 32;
+        const int wg = (int)xcd_linear_index(item, n_work);
+        const int sweep = wg / (kSweepRows * n_cg);
+        const int in_sweep = wg % (kSweepRows * n_cg);
+        const int rows_here = n_rb - sweep * kSweepRows < kSweepRows ? n_rb - sweep * kSweepRows
+                                                                      : kSweepRows;
+        const int bi = sweep * kSweepRows + in_sweep % rows_here;
+        const int bj = (in_sweep / rows_here) * kWaves + (threadIdx.x >> 6);
+        const int i0 = bi * 32, j0 = bj * 32;
+        if (j0 >= n_out) continue;                                 // wave-uniform; no barriers
+        const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
+        const int cols = n_out - j0 < 32 ? n_out - j0 : 32;
+        const int n_ks = a.n_ks;
+        const int jl = lane & 31;
+        const int il0 = 4 * (lane >> 5);
 
-    // ---- requests that do not depend on the contraction -----------------------------------
-    const rsrc_t rp = make_rsrc(a.pij + (int64_t)i0 * n_out, (uint32_t)rows * n_out * 4u);
-    const uint32_t o0 = ((uint32_t)il0 * n_out + j0 + jl) * 4u;
-    float pold[16];
+        // ---- requests that do not depend on the contraction -----------------------------------
+        const rsrc_t rp = make_rsrc(a.pij + (int64_t)i0 * n_out, (uint32_t)rows * n_out * 4u);
+        const uint32_t o0 = ((uint32_t)il0 * n_out + j0 + jl) * 4u;
+        float pold[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-        pold[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-            rp, o0 + (uint32_t)(8 * (r >> 2) + (r & 3)) * n_out * 4u, 0, 0));
-    // marginal inputs: lanes 0..31 the block's row units, 32..63 its column units (clamped)
-    const bool is_row = lane < 32;
-    const int u = is_row ? i0 + (lane < rows ? lane : rows - 1)
-                         : j0 + (lane - 32 < cols ? lane - 32 : cols - 1);
-    const float* sums = is_row ? a.ops.x_sum : a.ops.t_sum;
-    const int64_t st = is_row ? n_in : n_out;
-    float part[kSums];
+        for (int r = 0; r < 16; ++r)
+            pold[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                rp, o0 + (uint32_t)(8 * (r >> 2) + (r & 3)) * n_out * 4u, 0, 0));
+        // lanes 0..31 the block's row units, 32..63 its column units (clamped)
+        const bool is_row = lane < 32;
+        const int u = is_row ? i0 + (lane < rows ? lane : rows - 1)
+                             : j0 + (lane - 32 < cols ? lane - 32 : cols - 1);
+        // Mask of the lane's column over the block's 32 rows, one bit per row.  HCU of every row /
+        // column unit, spread by lane reads.  When the block's columns fall in at most two hidden
+        // HCUs (always for M_out >= 32), lane l reads the byte of row l % 32 and hidden HCU
+        // hc0 + l / 32, and one ballot gives both HCUs' row masks; otherwise every lane reads the
+        // bytes of its 16 elements.
+        const int hu = is_row ? u / g.in_mcu : u / g.out_mcu;
+        const int hj = __shfl(hu, 32 + jl, 64);
+        const int hc0 = __shfl(hu, 32, 64), hc1 = __shfl(hu, 63, 64);
+        uint32_t act_bits = 0;
+        if (hc1 - hc0 <= 1) {                                      // wave-uniform
+            const int hr = __shfl(hu, jl, 64);
+            const int hc = hc0 + (lane >> 5) < hc1 ? hc0 + (lane >> 5) : hc1;
+            const uint64_t bits = __ballot(a.mask[(int64_t)hr * g.out_hcu + hc] != 0);
+            act_bits = hj == hc0 ? (uint32_t)bits : (uint32_t)(bits >> 32);
+        } else {
 #pragma unroll
-    for (int q = 0; q < kSums; ++q) part[q] = sums[(q < nk ? q : nk - 1) * st + u];
-    const float p_old = is_row ? a.pi_old[u] : a.pj_old[u];
-    // Mask of the lane's column over the block's 32 rows, one bit per row.  HCU of every row /
-    // column unit, spread by lane reads.  When the block's columns fall in at most two hidden
-    // HCUs (always for M_out >= 32), lane l reads the byte of row l % 32 and hidden HCU
-    // hc0 + l / 32, and one ballot gives both HCUs' row masks; otherwise every lane reads the
-    // bytes of its 16 elements.
-    const int hu = is_row ? u / g.in_mcu : u / g.out_mcu;
-    const int hj = __shfl(hu, 32 + jl, 64);
-    const int hc0 = __shfl(hu, 32, 64), hc1 = __shfl(hu, 63, 64);
-    uint32_t act_bits = 0;
-    if (hc1 - hc0 <= 1) {                                      // wave-uniform
-        const int hr = __shfl(hu, jl, 64);
-        const int hc = hc0 + (lane >> 5) < hc1 ? hc0 + (lane >> 5) : hc1;
-        const uint64_t bits = __ballot(a.mask[(int64_t)hr * g.out_hcu + hc] != 0);
-        act_bits = hj == hc0 ? (uint32_t)bits : (uint32_t)(bits >> 32);
-    } else {
+            for (int r = 0; r < 16; ++r) {
+                const int il = il0 + 8 * (r >> 2) + (r & 3);
+                const int hi = __shfl(hu, il, 64);
+                act_bits |= (a.mask[(int64_t)hi * g.out_hcu + hj] != 0 ? 1u : 0u) << il;
+            }
+        }
+
+        // ---- per batch: contraction (operands straight from the fragment-order arrays), update --
+        const int64_t fa = ((int64_t)bi * n_ks * 64 + lane) * 8;
+        const int64_t fb = ((int64_t)bj * n_ks * 64 + lane) * 8;
+        for (int t = 0; t < a.n_batches; ++t) {
+            const SweepBatch bt = a.bt[t];
+            const int nk = bt.nk;
+            f16v acc = {};
+            for (int k0 = 0; k0 < nk; k0 += kChunk) {
+                u32x4 op[kChunk][4];
+#pragma unroll
+                for (int c = 0; c < kChunk; ++c) {
+                    const int64_t ks = (int64_t)(k0 + c < nk ? k0 + c : nk - 1) * 512;
+                    op[c][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa + ks);
+                    op[c][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa + ks);
+                    op[c][2] = *reinterpret_cast<const u32x4*>(bt.t_hi + fb + ks);
+                    op[c][3] = *reinterpret_cast<const u32x4*>(bt.t_lo + fb + ks);
+                }
+#pragma unroll
+                for (int c = 0; c < kChunk; ++c) {
+                    if (k0 + c < nk) {
+                        const bf8 ah = __builtin_bit_cast(bf8, op[c][0]);
+                        const bf8 al = __builtin_bit_cast(bf8, op[c][1]);
+                        const bf8 bh = __builtin_bit_cast(bf8, op[c][2]);
+                        const bf8 bl = __builtin_bit_cast(bf8, op[c][3]);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc, 0, 0, 0);
+                    }
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                pold[r] = to_storage<kDropBits>(fmaf(bt.c2, acc[r], bt.c1 * pold[r]));
+        }
+
+        // ---- epilogue: the elements of silent blocks, 16 unconditional buffer stores ----------
+        const bool jok = jl < cols;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int il = il0 + 8 * (r >> 2) + (r & 3);
-            const int hi = __shfl(hu, il, 64);
-            act_bits |= (a.mask[(int64_t)hi * g.out_hcu + hj] != 0 ? 1u : 0u) << il;
+            const uint32_t off = o0 + (uint32_t)(8 * (r >> 2) + (r & 3)) * n_out * 4u;
+            const bool keep = jok && !((act_bits >> il) & 1u);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pold[r]), rp,
+                                                  keep ? off : kDrop, 0, 0);
         }
     }
+}
+// Active blocks: one workgroup per (hidden HCU, 32 of its active input units, 4 column blocks
+// of the HCU), one wave per 32 x 32 block; workgroups past n_work store the marginal traces and
+// bias of every unit instead.
+template <int kDropBits>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_list,
+                    const int32_t* __restrict__ act_count, int n_rt, int n_cgr, int n_work) {
+    const int n_in = (int)g.n_in, n_out = (int)g.n_out;
+    const int nk = (a.B + 15) / 16;
+    const int n_ks = a.ops.n_ks;
+    if ((int)blockIdx.x >= n_work) {
+        const int64_t v = (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x;
+        if (v >= (int64_t)n_in + n_out) return;
+        const bool is_row = v < n_in;
+        const int u = is_row ? (int)v : (int)(v - n_in);
+        const float* sums = is_row ? a.ops.x_sum : a.ops.t_sum;
+        const int64_t st = is_row ? n_in : n_out;
+        MarginalIn m;
+        marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
+        const float p = marginal_value(m, sums, st, u, nk, a);
+        if (is_row) {
+            a.pi_new[u] = p;
+        } else {
+            a.pj_new[u] = p;
+            a.b[u] = a.bias_gain * fast_log(fmaxf(p, a.eps));
+        }
+        return;
+    }
+    const int lane = threadIdx.x & 63;
+    const int wg = (int)xcd_linear_index(blockIdx.x, n_work);
+    const int per_hcu = n_rt * n_cgr;
+    const int hj = wg / per_hcu;
+    const int rt = (wg - hj * per_hcu) / n_cgr;
+    const int c0 = ((wg - hj * per_hcu - rt * n_cgr) * kWaves + (threadIdx.x >> 6)) * 32;
+    const int k_total = act_count[hj] * g.in_mcu;
+    if (c0 >= g.out_mcu || rt * 32 >= k_total) return;         // wave-uniform; no barriers
+    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;
+    const int cols = g.out_mcu - c0 < 32 ? g.out_mcu - c0 : 32;
+    const int j0 = hj * g.out_mcu + c0;
+    const int jl = lane & 31;
+    const int il0 = 4 * (lane >> 5);
 
-    // ---- contraction: operands straight from the fragment-order arrays -----------------------
-    const int64_t fa = ((int64_t)bi * n_ks * 64 + lane) * 8;
-    const int64_t fb = ((int64_t)bj * n_ks * 64 + lane) * 8;
-    f16v acc = {};
-    for (int k0 = 0; k0 < nk; k0 += kChunk) {
-        u32x4 op[kChunk][4];
+    // unit of block row jl (the A-operand row of this lane) and the lane's column (clamped)
+    const int kr = rt * 32 + (jl < rows ? jl : rows - 1);
+    const int ua = act_list[(int64_t)hj * g.in_hcu + kr / g.in_mcu] * g.in_mcu + kr % g.in_mcu;
+    const int jb = j0 + (jl < cols ? jl : cols - 1);
+
+    // ---- requests that do not depend on the contraction -----------------------------------
+    float pold[16];
 #pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
-            const int64_t ks = (int64_t)(k0 + c < nk ? k0 + c : nk - 1) * 512;
-            op[c][0] = *reinterpret_cast<const u32x4*>(a.ops.x_hi + fa + ks);
-            op[c][1] = *reinterpret_cast<const u32x4*>(a.ops.x_lo + fa + ks);
-            op[c][2] = *reinterpret_cast<const u32x4*>(a.ops.t_hi + fb + ks);
-            op[c][3] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb + ks);
+    for (int r = 0; r < 16; ++r) {
+        const int ur = __shfl(ua, il0 + 8 * (r >> 2) + (r & 3), 64);
+        pold[r] = a.pij[(int64_t)ur * n_out + jb];
+    }
+    // marginal inputs: lanes 0..31 the block's row units, 32..63 its column units
+    const bool is_row = lane < 32;
+    const int u = is_row ? ua : jb;
+    const float* sums = is_row ? a.ops.x_sum : a.ops.t_sum;
+    const int64_t st = is_row ? n_in : n_out;
+    MarginalIn m;
+    marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
+
+    // ---- contraction: 16-byte fragment pieces of the gathered rows and of the columns --------
+    const int h = lane >> 5;
+    f16v acc = {};
+    for (int k0 = 0; k0 < nk; k0 += kActiveChunk) {
+        u32x4 op[kActiveChunk][4];
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            const int ks = k0 + c < nk ? k0 + c : nk - 1;
+            const int64_t fa = frag_chunk(ua, ks, h, n_ks), fb = frag_chunk(jb, ks, h, n_ks);
+            op[c][0] = *reinterpret_cast<const u32x4*>(a.ops.x_hi + fa);
+            op[c][1] = *reinterpret_cast<const u32x4*>(a.ops.x_lo + fa);
+            op[c][2] = *reinterpret_cast<const u32x4*>(a.ops.t_hi + fb);
+            op[c][3] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb);
         }
 #pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
+        for (int c = 0; c < kActiveChunk; ++c) {
             if (k0 + c < nk) {
                 const bf8 ah = __builtin_bit_cast(bf8, op[c][0]);
                 const bf8 al = __builtin_bit_cast(bf8, op[c][1]);
@@ -178,52 +319,71 @@ trace_kernel(Geometry g, TraceArgs a, int n_cg) {
     }
 
     // ---- marginal traces of the block's rows and columns, and their logs --------------------
-    float colsum = 0.0f;
-#pragma unroll
-    for (int q = 0; q < kSums; ++q)
-        if (q < nk) colsum += part[q];
-    for (int q = kSums; q < nk; ++q) colsum += sums[q * st + u];     // batches above 128
-    const float p = fmaf(a.a_eff, colsum * a.inv_b, a.c1 * p_old);
-    const float lp = fast_log(fmaxf(p, a.eps));
-    if (is_row && lane < rows && bj == 0) a.pi_new[u] = p;
-    if (!is_row && lane - 32 < cols && bi == 0) {
-        a.pj_new[u] = p;
-        a.b[u] = a.bias_gain * lp;
-    }
+    const float lp = fast_log(fmaxf(marginal_value(m, sums, st, u, nk, a), a.eps));
     const float lpj = __shfl(lp, 32 + jl, 64);
 
-    // ---- epilogue: joint trace and masked weights, 32 unconditional buffer stores per lane ----
+    // ---- epilogue: joint trace and weight of every element of the block ----------------------
     const bool jok = jl < cols;
-    const rsrc_t rw = make_rsrc(a.w + (int64_t)i0 * n_out, (uint32_t)rows * n_out * 4u);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int il = il0 + 8 * (r >> 2) + (r & 3);
+        const int ur = __shfl(ua, il, 64);
         const float lpi = __shfl(lp, il, 64);
-        const uint32_t off = o0 + (uint32_t)(8 * (r >> 2) + (r & 3)) * n_out * 4u;
         const float pn = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pold[r]));
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pn), rp, jok ? off : kDrop, 0, 0);
         const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(wv), rw,
-                                              jok && ((act_bits >> il) & 1u) ? off : kDrop, 0, 0);
+        if (jok && il < rows) {
+            const int64_t e = (int64_t)ur * n_out + jb;
+            a.pij[e] = pn;
+            a.w[e] = wv;
+        }
     }
 }
 
 }  // namespace
 
-hipError_t launch_trace_update(hipStream_t stream, const Geometry& g, const TraceArgs& a,
-                               hipEvent_t start, hipEvent_t stop) {
+hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const SweepArgs& a,
+                              int64_t resident_wgs, hipEvent_t start, hipEvent_t stop) {
+    if (a.n_batches < 1 || a.n_batches > kMaxSweepBatches) return hipErrorInvalidValue;
     const int64_t n_rb = (g.n_in + 31) / 32, n_cb = (g.n_out + 31) / 32;
     const int64_t n_cg = (n_cb + kWaves - 1) / kWaves;
-    void (*kernel)(Geometry, TraceArgs, int) = nullptr;
+    void (*kernel)(Geometry, SweepArgs, int, int) = nullptr;
     switch (a.drop_bits) {
-        case 0: kernel = trace_kernel<0>; break;
-        case 13: kernel = trace_kernel<13>; break;
-        case 16: kernel = trace_kernel<16>; break;
+        case 0: kernel = trace_sweep_kernel<0>; break;
+        case 13: kernel = trace_sweep_kernel<13>; break;
+        case 16: kernel = trace_sweep_kernel<16>; break;
         default: return hipErrorInvalidValue;
     }
+    const int64_t n_work = n_rb * n_cg;
+    int64_t grid = n_work;
+    if (resident_wgs > 0 && resident_wgs < grid) grid = (resident_wgs + 7) / 8 * 8;
     // the events (when given) are stamped by the dispatch itself, so they time the kernel alone
-    hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_rb * n_cg)), dim3(kWaves * 64), 0, stream,
-                          start, stop, 0, g, a, (int)n_cg);
+    hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kWaves * 64), 0, stream, start,
+                          stop, 0, g, a, (int)n_cg, (int)n_work);
+    return hipGetLastError();
+}
+
+int64_t trace_active_workgroups(const Geometry& g, int32_t max_active) {
+    const int64_t n_rt = ((int64_t)max_active * g.in_mcu + 31) / 32;
+    const int64_t n_cgr = ((g.out_mcu + 31) / 32 + kWaves - 1) / kWaves;
+    return (int64_t)g.out_hcu * n_rt * n_cgr + (g.n_in + g.n_out + kWaves * 64 - 1) / (kWaves * 64);
+}
+
+hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const TraceArgs& a,
+                               const int32_t* act_list, const int32_t* act_count,
+                               int32_t max_active, hipEvent_t start, hipEvent_t stop) {
+    const int64_t n_rt = ((int64_t)max_active * g.in_mcu + 31) / 32;
+    const int64_t n_cgr = ((g.out_mcu + 31) / 32 + kWaves - 1) / kWaves;
+    const int64_t n_work = (int64_t)g.out_hcu * n_rt * n_cgr;
+    const int64_t blocks = trace_active_workgroups(g, max_active);
+    void (*kernel)(Geometry, TraceArgs, const int32_t*, const int32_t*, int, int, int) = nullptr;
+    switch (a.drop_bits) {
+        case 0: kernel = trace_active_kernel<0>; break;
+        case 13: kernel = trace_active_kernel<13>; break;
+        case 16: kernel = trace_active_kernel<16>; break;
+        default: return hipErrorInvalidValue;
+    }
+    hipExtLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kWaves * 64), 0, stream, start,
+                          stop, 0, g, a, act_list, act_count, (int)n_rt, (int)n_cgr, (int)n_work);
     return hipGetLastError();
 }
 

@@ -1,0 +1,79 @@
+"""The deferred sweep over silent elements.
+
+The library updates the Pij elements of active blocks every batch, and those of silent blocks
+(which the support never reads) for several consecutive batches in one sweep on a second
+stream, each batch's update applied in order with the same rounding.  Grouping must therefore
+be invisible: the state after a run is bitwise the same whether the sweeps cover four batches
+or one (reading the state applies the pending ones), and a multi-batch run without
+re-synchronisation agrees with the oracle's per-batch updates.
+"""
+import numpy as np
+import pytest
+
+from paper_2106_05373_amd import synth
+
+from pairs import TOL_ACT, Pair, assert_state_close, bcpnn, max_abs, workload_config, workload_mask
+
+pytestmark = pytest.mark.gpu
+
+MNIST = synth.WORKLOADS["mnist"]
+# 11 batches of mixed sizes (a 17-row batch has a partial 16-row k-step): sweeps of 4, 4, 3
+SIZES = [128, 128, 64, 128, 128, 128, 96, 128, 128, 17, 128]
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print(f"\n[gpu case] {request.node.nodeid}", flush=True)
+    yield
+
+
+def _inputs():
+    px, _ = synth.dataset(MNIST, n=sum(SIZES))
+    X = synth.encode_pixels(px)
+    out, k = [], 0
+    for b in SIZES:
+        out.append(X[k:k + b])
+        k += b
+    return out
+
+
+def test_sweep_grouping_is_bitwise_invisible():
+    """The same batches, with a structural update before the sixth, run freely and with the
+    state read after every batch: bitwise identical states."""
+    import torch
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()]
+    states = []
+    for read_each in (False, True):
+        layer = bcpnn().Layer(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
+        for k, x in enumerate(xs):
+            if k == 5:
+                layer.structural_update(count=False)
+            layer.train_batch(x)
+            if read_each:
+                layer.get_state(("pij",))
+        states.append(layer.get_state())
+        layer.close()
+    for key in states[0]:
+        assert np.array_equal(states[0][key].view(np.uint8), states[1][key].view(np.uint8)), key
+
+
+def test_multi_batch_run_matches_oracle():
+    """Target-clamped batches (the traces then depend on the inputs alone, with no feedback
+    through the weights), no re-synchronisation: after 11 batches the state agrees with the
+    oracle to the per-step tolerances; a forward pass mid-run does not disturb the sweeps."""
+    rng = np.random.default_rng(5)
+    pair = Pair(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
+    cfg = pair.cfg
+    t = pair.torch
+    for k, x in enumerate(_inputs()):
+        win = rng.integers(0, cfg.out_mcu, size=(x.shape[0], cfg.out_hcu))
+        target = np.zeros((x.shape[0], cfg.out_hcu, cfg.out_mcu), np.float32)
+        np.put_along_axis(target, win[..., None], 1.0, axis=-1)
+        pair.train(x, target.reshape(x.shape[0], -1))
+        if k == 6:
+            y = t.empty((x.shape[0], pair.n_out), device="cuda", dtype=t.float32)
+            pair.gpu.forward(pair.dev(x), y)
+            _, y_o = pair.ora.forward(x)
+            assert max_abs(y.cpu().numpy(), y_o) <= TOL_ACT
+    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="after 11 batches")
+    pair.close()
