@@ -42,6 +42,7 @@ SWEEP_BATCHES = 4
 # sources it was measured on (the trace kernels and the support kernel, which writes their
 # operands).  A changed kernel reports null until measured again.
 MEASURED_TRAFFIC = {
+    ("mnist", "e8ab3fd0c86c58f7ddae36d080627500f14884f9095eafc0788a89d8a296633a"): 74526360,
 }
 
 
@@ -162,8 +163,9 @@ def main():
         step(s)
     torch.cuda.synchronize()
 
-    layer.profile_enable(PROFILE_PERIOD)
-    layer.profile_read()                          # discard anything recorded so far
+    layer.profile_read()                          # applies pending sweeps; discards old timings
+    # every PROFILE_PERIOD-th sweep of a long run, every sweep of a short one
+    layer.profile_enable(PROFILE_PERIOD if args.steps >= 64 * PROFILE_PERIOD else 1)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -200,7 +202,9 @@ def main():
     pij_bytes = 4.0 * E + 4.0 * (E - active)
     ops_bytes = 4.0 * (L.n_in + L.n_out) * b_pad + 4.0 * (L.n_in + L.n_out) * (b_pad // 16)
     bytes_per_launch = pij_bytes + per_sweep * ops_bytes
-    avg_sweep_s = sweep_ms / 1e3 / max(sweep_launches, 1)
+    if sweep_launches == 0 or sweep_ms <= 0:
+        raise RuntimeError("no sweep launch was timed")
+    avg_sweep_s = sweep_ms / 1e3 / sweep_launches
     achieved_gbs = bytes_per_launch / avg_sweep_s / 1e9
     flops_per_launch = 2.0 * E * avg_b * per_sweep
     csrc = os.path.join(ROOT, "paper_2106_05373_amd", "csrc")
@@ -212,9 +216,11 @@ def main():
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
         "kernel": "trace_sweep_kernel (silent elements of Pij: the x^T t contractions of up to "
                   f"{SWEEP_BATCHES} consecutive batches on split-bf16 MFMA, one read and one write "
-                  "of Pij; one workgroup per CU on a second stream, overlapping later batches)",
+                  "of Pij; on a second stream overlapping later batches, one workgroup per CU "
+                  "for a small layer)",
         "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_launches,
-        "timed_every": PROFILE_PERIOD, "batches_per_launch": round(per_sweep, 3),
+        "timed_every": PROFILE_PERIOD if args.steps >= 64 * PROFILE_PERIOD else 1,
+        "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
         "contraction_tflops": round(flops_per_launch / avg_sweep_s / 1e12, 3),
     }

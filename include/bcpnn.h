@@ -33,6 +33,14 @@
  * structural_update with a non-NULL count pointer, which wait for the stream.  Calls on one
  * layer must not run concurrently from several host threads.
  *
+ * Second stream: train_batch updates, on the caller's stream, everything the next batch reads
+ * (Pij and w of active blocks, Pi, Pj, b, the activities).  The Pij of silent blocks are
+ * updated on a stream the layer owns (default priority, non-blocking), for up to four batches
+ * in one pass with the same per-batch arithmetic; the caller's stream is made to wait for that
+ * work before every call that reads or replaces Pij (get_state, set_state, structural_update,
+ * recompute_weights, profile_read) and destroy waits for both streams.  The results are those
+ * of per-batch updates, bit for bit.
+ *
  * Errors: every call returns a bcpnn_status.  Arguments are checked on the host before any
  * device work; BCPNN_EINVAL leaves the layer unchanged.  A failed HIP call returns
  * BCPNN_EDEVICE and marks the layer failed: later calls on it return BCPNN_ESTATE (destroy
@@ -149,12 +157,14 @@ bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in
  * to the host.  Waits.  EINVAL before the first structural update. */
 bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
 
-/* Kernel timing for measurement: with period n > 0, every n-th launch of the joint-trace kernel
- * (counting from the call) carries a pair of HIP events stamped by the dispatch itself
+/* Kernel timing for measurement: with period n > 0, every n-th launch of the silent-block sweep
+ * of the joint traces (of the active-block trace kernel when the mask has no silent block),
+ * counting from the call, carries a pair of HIP events stamped by the dispatch itself
  * (hipExtLaunchKernel), so they bracket the kernel's execution alone; n = 0 turns it off.  Each
  * timed launch costs the stream a few microseconds of dispatch, so a period of 10 or more
- * keeps a throughput measurement nearly unperturbed.  bcpnn_profile_read waits for the stream
- * and returns the summed duration (ms) and count of the timed launches since the last read.
+ * keeps a throughput measurement nearly unperturbed.  bcpnn_profile_read applies the pending
+ * silent updates, waits for both streams and returns the summed duration (ms) and count of the
+ * timed launches since the last read.
  * Errors: EINVAL for n < 0. */
 bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);

@@ -21,6 +21,8 @@ constexpr int32_t kMaxInHcu = 49152;     // mask column held in LDS by the swap 
 constexpr int32_t kMaxSwaps = 256;
 // operand sets: one group filling, up to two being swept
 constexpr int kSets = 3 * bcpnn::kMaxSweepBatches;
+// 32 x 32 blocks of Pij per CU up to which the sweep runs with one workgroup per CU
+constexpr int64_t kSmallSweepBlocksPerCu = 64;
 
 thread_local std::string g_error;
 
@@ -342,13 +344,16 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = hipEventCreateWithFlags(&L->sweep_ready, hipEventDisableTiming);
     // default priority; non-blocking, so that it never waits for a legacy default stream
     if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
-    // The sweep keeps one workgroup (one wave per SIMD) resident per CU, which leaves room on
-    // every CU for the support and active-block workgroups of the batches it overlaps.
+    // A small layer's sweep keeps one workgroup (one wave per SIMD) resident per CU, which
+    // leaves room on every CU for the support and active-block workgroups of the batches it
+    // overlaps, and still finishes within them.  A large layer's sweep is the longer stream;
+    // it takes the whole machine (one workgroup per block group).
     int dev = 0, n_cu = 0;
     if (e == hipSuccess) e = hipGetDevice(&dev);
     if (e == hipSuccess)
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e == hipSuccess) L->sweep_wgs = n_cu;
+    const int64_t blocks = ((g.n_in + 31) / 32) * ((g.n_out + 31) / 32);
+    if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : 0;
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,

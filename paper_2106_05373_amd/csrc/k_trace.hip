@@ -91,6 +91,15 @@ __device__ __forceinline__ float to_storage(float v) {
     }
 }
 
+// Value of lane src in lanes 0..31 and of lane src + 4 in lanes 32..63 (src a constant).
+template <typename T>
+__device__ __forceinline__ T half_broadcast(T v, int src, int lane) {
+    const int bits = __builtin_bit_cast(int, v);
+    const int lo = __builtin_amdgcn_readlane(bits, src);
+    const int hi = __builtin_amdgcn_readlane(bits, src + 4);
+    return __builtin_bit_cast(T, lane < 32 ? lo : hi);
+}
+
 // Inputs of one unit's marginal trace: its column sums over the batch's 16-row tiles (the
 // first kSums requested up front) and its previous value.
 struct MarginalIn {
@@ -262,26 +271,69 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
     const int hj = wg / per_hcu;
     const int rt = (wg - hj * per_hcu) / n_cgr;
     const int c0 = ((wg - hj * per_hcu - rt * n_cgr) * kWaves + (threadIdx.x >> 6)) * 32;
-    const int k_total = act_count[hj] * g.in_mcu;
-    if (c0 >= g.out_mcu || rt * 32 >= k_total) return;         // wave-uniform; no barriers
-    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;
+    if (c0 >= g.out_mcu) return;                               // wave-uniform; no barriers
     const int cols = g.out_mcu - c0 < 32 ? g.out_mcu - c0 : 32;
     const int j0 = hj * g.out_mcu + c0;
     const int jl = lane & 31;
     const int il0 = 4 * (lane >> 5);
+    const int h = lane >> 5;
+    const int jb = j0 + (jl < cols ? jl : cols - 1);          // the lane's column (clamped)
 
-    // unit of block row jl (the A-operand row of this lane) and the lane's column (clamped)
-    const int kr = rt * 32 + (jl < rows ? jl : rows - 1);
-    const int ua = act_list[(int64_t)hj * g.in_hcu + kr / g.in_mcu] * g.in_mcu + kr % g.in_mcu;
-    const int jb = j0 + (jl < cols ? jl : cols - 1);
+    // ---- requests, in order of dependence -------------------------------------------------
+    // The active count and the list entry of block row jl are requested together (rows past
+    // the count read an in-bounds entry and are never stored), then everything on the column
+    // side, which needs neither.
+    const int k_total = act_count[hj] * g.in_mcu;
+    const int n_units = g.in_hcu * g.in_mcu;
+    const int kr = rt * 32 + jl < n_units ? rt * 32 + jl : n_units - 1;
+    const int hsel = act_list[(int64_t)hj * g.in_hcu + kr / g.in_mcu];
+    u32x4 opt[kActiveChunk][2], opx[kActiveChunk][2];
+    auto load_t = [&](int k0) {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            const int64_t fb = frag_chunk(jb, k0 + c < nk ? k0 + c : nk - 1, h, n_ks);
+            opt[c][0] = *reinterpret_cast<const u32x4*>(a.ops.t_hi + fb);
+            opt[c][1] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb);
+        }
+    };
+    auto load_x = [&](int k0, int ua) {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            const int64_t fa = frag_chunk(ua, k0 + c < nk ? k0 + c : nk - 1, h, n_ks);
+            opx[c][0] = *reinterpret_cast<const u32x4*>(a.ops.x_hi + fa);
+            opx[c][1] = *reinterpret_cast<const u32x4*>(a.ops.x_lo + fa);
+        }
+    };
+    f16v acc = {};
+    auto contract = [&](int k0) {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            if (k0 + c < nk) {
+                const bf8 ah = __builtin_bit_cast(bf8, opx[c][0]);
+                const bf8 al = __builtin_bit_cast(bf8, opx[c][1]);
+                const bf8 bh = __builtin_bit_cast(bf8, opt[c][0]);
+                const bf8 bl = __builtin_bit_cast(bf8, opt[c][1]);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc, 0, 0, 0);
+            }
+        }
+    };
+    load_t(0);
 
-    // ---- requests that do not depend on the contraction -----------------------------------
+    // unit of block row jl (the A-operand row of this lane), clamped into the layer
+    const int hs = hsel < 0 ? 0 : (hsel < g.in_hcu ? hsel : g.in_hcu - 1);
+    const int ua = hs * g.in_mcu + kr % g.in_mcu;
+    // Row of result register r: 8 (r / 4) + r % 4 in lanes 0..31, 4 more in lanes 32..63, so
+    // its unit is a broadcast of one lane per half-wave (two lane reads, no permute).
+    int ur[16];
     float pold[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-        const int ur = __shfl(ua, il0 + 8 * (r >> 2) + (r & 3), 64);
-        pold[r] = a.pij[(int64_t)ur * n_out + jb];
+        ur[r] = half_broadcast(ua, 8 * (r >> 2) + (r & 3), lane);
+        pold[r] = a.pij[(int64_t)ur[r] * n_out + jb];
     }
+    load_x(0, ua);
     // marginal inputs: lanes 0..31 the block's row units, 32..63 its column units
     const bool is_row = lane < 32;
     const int u = is_row ? ua : jb;
@@ -291,32 +343,13 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
     marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
 
     // ---- contraction: 16-byte fragment pieces of the gathered rows and of the columns --------
-    const int h = lane >> 5;
-    f16v acc = {};
-    for (int k0 = 0; k0 < nk; k0 += kActiveChunk) {
-        u32x4 op[kActiveChunk][4];
-#pragma unroll
-        for (int c = 0; c < kActiveChunk; ++c) {
-            const int ks = k0 + c < nk ? k0 + c : nk - 1;
-            const int64_t fa = frag_chunk(ua, ks, h, n_ks), fb = frag_chunk(jb, ks, h, n_ks);
-            op[c][0] = *reinterpret_cast<const u32x4*>(a.ops.x_hi + fa);
-            op[c][1] = *reinterpret_cast<const u32x4*>(a.ops.x_lo + fa);
-            op[c][2] = *reinterpret_cast<const u32x4*>(a.ops.t_hi + fb);
-            op[c][3] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb);
-        }
-#pragma unroll
-        for (int c = 0; c < kActiveChunk; ++c) {
-            if (k0 + c < nk) {
-                const bf8 ah = __builtin_bit_cast(bf8, op[c][0]);
-                const bf8 al = __builtin_bit_cast(bf8, op[c][1]);
-                const bf8 bh = __builtin_bit_cast(bf8, op[c][2]);
-                const bf8 bl = __builtin_bit_cast(bf8, op[c][3]);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc, 0, 0, 0);
-            }
-        }
+    contract(0);
+    for (int k0 = kActiveChunk; k0 < nk; k0 += kActiveChunk) {   // batches above 128 rows
+        load_t(k0);
+        load_x(k0, ua);
+        contract(k0);
     }
+    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
 
     // ---- marginal traces of the block's rows and columns, and their logs --------------------
     const float lp = fast_log(fmaxf(marginal_value(m, sums, st, u, nk, a), a.eps));
@@ -327,12 +360,11 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         const int il = il0 + 8 * (r >> 2) + (r & 3);
-        const int ur = __shfl(ua, il, 64);
-        const float lpi = __shfl(lp, il, 64);
+        const float lpi = half_broadcast(lp, 8 * (r >> 2) + (r & 3), lane);
         const float pn = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pold[r]));
         const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
         if (jok && il < rows) {
-            const int64_t e = (int64_t)ur * n_out + jb;
+            const int64_t e = (int64_t)ur[r] * n_out + jb;
             a.pij[e] = pn;
             a.w[e] = wv;
         }
