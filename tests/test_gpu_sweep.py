@@ -77,3 +77,48 @@ def test_multi_batch_run_matches_oracle():
             assert max_abs(y.cpu().numpy(), y_o) <= TOL_ACT
     assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="after 11 batches")
     pair.close()
+
+
+def test_state_calls_between_batches_see_every_update():
+    """Calls that touch the traces, made while a group of silent updates is still queued:
+    recompute_weights, readout and set_state in the middle of a run, and destroy right after
+    batches, leave the layer as per-batch updates would.  The reference run reads the state
+    after every batch; the other interleaves the calls at the same points."""
+    import torch
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()]
+    cfg = workload_config(MNIST, alpha=0.02)
+    mask = workload_mask(MNIST)
+
+    ref = bcpnn().Layer(cfg, mask)
+    snap = None
+    for k, x in enumerate(xs):
+        ref.train_batch(x)
+        if k == 2:
+            snap = ref.get_state()                   # the state set_state re-applies below
+        if k == 4:
+            ref.recompute_weights()
+    st_ref = ref.get_state()
+    ref.close()
+
+    lay = bcpnn().Layer(cfg, mask)
+    win = torch.empty((xs[0].shape[0], cfg.out_hcu), device="cuda", dtype=torch.int32)
+    for k, x in enumerate(xs):
+        lay.train_batch(x)
+        if k == 1:
+            lay.readout(xs[0], win)                  # reads w, b only; the queue stays
+        if k == 2:
+            lay.set_state(snap)                      # applies the queue, then replaces
+        if k == 4:
+            lay.recompute_weights()
+    st = lay.get_state()
+    lay.close()
+    for key in st_ref:
+        assert np.array_equal(st_ref[key].view(np.uint8), st[key].view(np.uint8)), key
+
+    # destroy with queued silent updates (waits for both streams, no leak, no fault)
+    for _ in range(3):
+        tmp = bcpnn().Layer(cfg, mask)
+        for x in xs[:6]:
+            tmp.train_batch(x)
+        tmp.close()
+    torch.cuda.synchronize()
