@@ -42,7 +42,7 @@ SWEEP_BATCHES = 4
 # sources it was measured on (the trace kernels and the support kernel, which writes their
 # operands).  A changed kernel reports null until measured again.
 MEASURED_TRAFFIC = {
-    ("mnist", "e8ab3fd0c86c58f7ddae36d080627500f14884f9095eafc0788a89d8a296633a"): 74526360,
+    ("mnist", "3e74d45ce8cdc0b4d3bb6a7f06481015593d7838cf0966ea40f9503b52f496ae"): 74865756,
 }
 
 
@@ -214,10 +214,11 @@ def main():
     roofline = {
         "bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS,
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
-        "kernel": "trace_sweep_kernel (silent elements of Pij: the x^T t contractions of up to "
+        "kernel": "silent-block trace sweep (the x^T t contractions of up to "
                   f"{SWEEP_BATCHES} consecutive batches on split-bf16 MFMA, one read and one write "
-                  "of Pij; on a second stream overlapping later batches, one workgroup per CU "
-                  "for a small layer)",
+                  "of Pij; on a second stream overlapping later batches: trace_sweep_kernel, one "
+                  "workgroup per CU, for a small layer, trace_sweep_tile_kernel, 128x128 "
+                  "LDS-staged tiles, for a large one)",
         "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_launches,
         "timed_every": PROFILE_PERIOD if args.steps >= 64 * PROFILE_PERIOD else 1,
         "batches_per_launch": round(per_sweep, 3),

@@ -71,7 +71,7 @@ struct bcpnn_layer {
     int64_t n_sweeps = 0;                // sweeps enqueued; sweep k records sweep_done[k % kSets]
     int64_t waited = -1;                 // the caller's stream already waits for sweeps <= this
     bool full_mask = false;              // no silent block: no sweeps
-    int64_t sweep_wgs = 0;               // resident workgroups of a sweep (one per CU)
+    int64_t sweep_wgs = 0;               // sweep launch: one workgroup per CU, or -1 (tiles)
     bool mi_valid = false;
     bool failed = false;
     int32_t profile_every = 0;           // 0: off; n: every n-th sweep launch carries events
@@ -347,13 +347,13 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     // A small layer's sweep keeps one workgroup (one wave per SIMD) resident per CU, which
     // leaves room on every CU for the support and active-block workgroups of the batches it
     // overlaps, and still finishes within them.  A large layer's sweep is the longer stream;
-    // it takes the whole machine (one workgroup per block group).
+    // it takes the whole machine in 128 x 128 tiles with operands staged through LDS.
     int dev = 0, n_cu = 0;
     if (e == hipSuccess) e = hipGetDevice(&dev);
     if (e == hipSuccess)
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t blocks = ((g.n_in + 31) / 32) * ((g.n_out + 31) / 32);
-    if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : 0;
+    if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : -1;
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,

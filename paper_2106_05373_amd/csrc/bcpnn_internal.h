@@ -127,7 +127,8 @@ struct SweepArgs {
     int drop_bits;
 };
 // resident_wgs > 0 caps the grid at that many workgroups (rounded up to a multiple of 8), each
-// looping over the 32 x 128 block groups; 0 launches one workgroup per group.
+// looping over the 32 x 128 block groups; 0 launches one workgroup per group; < 0 selects the
+// 128 x 128 LDS-staged tiles of a large layer.
 hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const SweepArgs& a,
                               int64_t resident_wgs, hipEvent_t start = nullptr,
                               hipEvent_t stop = nullptr);

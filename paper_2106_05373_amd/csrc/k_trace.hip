@@ -30,6 +30,9 @@
 //  * The support kernel of the same batch has already written x^T and t^T split, in MFMA
 //    fragment order (one 1 KiB chunk per 32 units and 16 batch rows), and the column sums of x
 //    and t per 16-row tile.
+//  * The sweep of a large layer (more than 64 blocks per CU) uses 128 x 128 workgroup tiles
+//    whose operands are staged through LDS (see trace_sweep_tile_kernel); everything else
+//    below describes the one-wave-per-block kernels.
 //  * Every wave owns one 32 x 32 block and works alone: no LDS staging, no barrier.  It
 //    requests its Pij values (and, in the active kernel, the inputs of its rows' and columns'
 //    marginal traces) first, then streams the operands straight into registers (each k-step of
@@ -237,6 +240,218 @@ trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work) {
         }
     }
 }
+// Mask of the lane's column over a 32 x 32 block's rows, one bit per row (rows i0 .. i0 + rows - 1,
+// columns j0 .. j0 + cols - 1), as in the sweep below: one byte per lane and one ballot when the
+// block's columns fall in at most two hidden HCUs, else the bytes of the lane's 16 elements.
+__device__ __forceinline__ uint32_t block_mask_bits(const Geometry& g, const uint8_t* mask,
+                                                    int i0, int rows, int j0, int cols,
+                                                    int lane) {
+    const int jl = lane & 31;
+    const int il0 = 4 * (lane >> 5);
+    const bool is_row = lane < 32;
+    const int u = is_row ? i0 + (lane < rows ? lane : rows - 1)
+                         : j0 + (lane - 32 < cols ? lane - 32 : cols - 1);
+    const int hu = is_row ? u / g.in_mcu : u / g.out_mcu;
+    const int hj = __shfl(hu, 32 + jl, 64);
+    const int hc0 = __shfl(hu, 32, 64), hc1 = __shfl(hu, 63, 64);
+    uint32_t bits32 = 0;
+    if (hc1 - hc0 <= 1) {                                          // wave-uniform
+        const int hr = __shfl(hu, jl, 64);
+        const int hc = hc0 + (lane >> 5) < hc1 ? hc0 + (lane >> 5) : hc1;
+        const uint64_t bits = __ballot(mask[(int64_t)hr * g.out_hcu + hc] != 0);
+        bits32 = hj == hc0 ? (uint32_t)bits : (uint32_t)(bits >> 32);
+    } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const int hi = __shfl(hu, il, 64);
+            bits32 |= (mask[(int64_t)hi * g.out_hcu + hj] != 0 ? 1u : 0u) << il;
+        }
+    }
+    return bits32;
+}
+
+// Silent sweep of a large layer: one 128 x 128 tile (4 x 4 blocks) per workgroup of four waves,
+// wave w on row block w of the tile and all four column blocks (64 accumulators).  Per k-step
+// the workgroup needs 16 KiB of operands (x of four row blocks, t of four column blocks, hi and
+// lo); each 1 KiB fragment chunk is copied straight into LDS by the memory unit
+// (global_load_lds, 16 bytes per lane) into one of kStages stage buffers of kKC k-steps, so
+// kStages - 1 chunks are in flight while one feeds the matrix cores, with one barrier per
+// chunk.  The chunk sequence runs over all the queued batches; after a batch's last chunk the
+// wave applies that batch's update to its Pij values in registers.  Operand traffic from L2 is
+// 16 bytes per element per batch of 256 (40 with one wave per block); every wave takes part in
+// every barrier (waves past the layer compute on clamped data and store nothing).
+// Measured on the STL-shaped layer (4 batches per launch): two stages of two k-steps 3.57 ms,
+// four of one 3.74 ms, three of two (one workgroup per CU) 6.85 ms; the one-wave-per-block
+// sweep 5.21 ms.
+constexpr int kTileKC = 2;
+constexpr int kTileStages = 2;
+__device__ __forceinline__ void stage_barrier() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// s_waitcnt immediate with vmcnt = n (6 bits) and the other counters left alone.
+constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+template <int kDropBits, int kKC, int kStages>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
+    constexpr int kItems = 16 * kKC;                // 1 KiB items per chunk
+    constexpr int kPerWave = kItems / kWaves;
+    __shared__ u32x4 stage[kStages][kItems][64];
+    // the wave index is uniform: make that visible, so the buffer resources built from it
+    // stay in scalar registers
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n_in = (int)g.n_in, n_out = (int)g.n_out;
+    const int n_rb = (n_in + 31) / 32, n_cb = (n_out + 31) / 32;
+    const int n_ti = (n_rb + 3) / 4;
+    constexpr int kSweepTiles = kSweepRows / 4;
+    const int wg = (int)xcd_linear_index(blockIdx.x, gridDim.x);
+    const int sweep = wg / (kSweepTiles * n_tj);
+    const int in_sweep = wg % (kSweepTiles * n_tj);
+    const int here = n_ti - sweep * kSweepTiles < kSweepTiles ? n_ti - sweep * kSweepTiles
+                                                              : kSweepTiles;
+    const int ti = sweep * kSweepTiles + in_sweep % here;
+    const int tj = in_sweep / here;
+    const int n_ks = a.n_ks;
+
+    // ---- requests that do not depend on the contraction (issued first) ----------------------
+    const int bi = 4 * ti + wave;
+    const int i0 = (bi < n_rb ? bi : n_rb - 1) * 32;
+    const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
+    const bool live = bi < n_rb;                           // wave-uniform
+    const int j00 = 4 * tj * 32;
+    const int jl = lane & 31, il0 = 4 * (lane >> 5);
+    const rsrc_t rp = make_rsrc(a.pij + (int64_t)i0 * n_out, (uint32_t)rows * n_out * 4u);
+    const uint32_t o0 = ((uint32_t)il0 * n_out + j00 + jl) * 4u;
+    float pold[4][16];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            pold[c][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                rp, o0 + (uint32_t)((8 * (r >> 2) + (r & 3)) * n_out + 32 * c) * 4u, 0, 0));
+    uint32_t act_bits[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int j0 = j00 + 32 * c;
+        const int jc = j0 < n_out ? j0 : (n_cb - 1) * 32;
+        act_bits[c] = block_mask_bits(g, a.mask, i0, rows, jc, n_out - jc < 32 ? n_out - jc : 32,
+                                      lane);
+    }
+
+    // chunk sequence over the queued batches
+    int n_ch = 0;
+    for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
+    // DMA of the chunk at (batch t, first k-step k0) into stage buffer sb: wave w issues items
+    // w, w + 4, ...; item = (k-step in chunk * 8 + operand block) * 2 + {hi, lo}, operand blocks
+    // 0..3 the tile's row blocks (x), 4..7 its column blocks (t)
+    auto dma = [&](int t, int k0, int sb) {
+        const SweepBatch bt = a.bt[t];
+#pragma unroll
+        for (int q = 0; q < kPerWave; ++q) {
+            const int item = wave + kWaves * q;
+            const int half = item & 1, ob = (item >> 1) & 7, kq = item >> 4;
+            int blk = ob < 4 ? 4 * ti + ob : 4 * tj + ob - 4;
+            const int nb = ob < 4 ? n_rb : n_cb;
+            blk = blk < nb ? blk : nb - 1;
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const uint16_t* base = ob < 4 ? (half ? bt.x_lo : bt.x_hi) : (half ? bt.t_lo : bt.t_hi);
+            const uint16_t* src = base + (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
+            __builtin_amdgcn_global_load_lds((const void*)src,
+                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+        }
+    };
+    auto next = [&](int& t, int& k0) {
+        k0 += kKC;
+        if (k0 >= a.bt[t].nk) { k0 = 0; ++t; }
+    };
+
+    // prologue: the first kStages - 1 chunks in flight
+    int dt = 0, dk = 0;                 // next chunk to request
+#pragma unroll
+    for (int q = 0; q < kStages - 1; ++q)
+        if (q < n_ch) {
+            dma(dt, dk, q);
+            next(dt, dk);
+        }
+
+    f16v acc[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] = f16v{};
+    int ct = 0, ck = 0;                 // chunk being computed
+    for (int lc = 0; lc < n_ch; ++lc) {
+        // this wave's requests for chunk lc are done once at most those of the later chunks in
+        // flight remain (requests complete in order); the barrier then makes chunk lc visible
+        // to every wave and tells that every wave has finished chunk lc - 1, whose buffer is
+        // refilled below
+        const int later = n_ch - 1 - lc < kStages - 2 ? n_ch - 1 - lc : kStages - 2;
+        if (later >= kStages - 2) __builtin_amdgcn_s_waitcnt(vm_wait((kStages - 2) * kPerWave));
+        else if (later == 2) __builtin_amdgcn_s_waitcnt(vm_wait(2 * kPerWave));
+        else if (later == 1) __builtin_amdgcn_s_waitcnt(vm_wait(kPerWave));
+        else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        stage_barrier();
+        if (lc + kStages - 1 < n_ch) {
+            dma(dt, dk, (lc + kStages - 1) % kStages);
+            next(dt, dk);
+        }
+        const int sb = lc % kStages;
+        const int nk = a.bt[ct].nk;
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            if (ck + kq < nk) {
+                const bf8 ah = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + wave) * 2][lane]);
+                const bf8 al = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + wave) * 2 + 1][lane]);
+                bf8 bh[4], bl[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + 4 + c) * 2][lane]);
+                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + 4 + c) * 2 + 1][lane]);
+                }
+                // the four accumulators interleaved, each still summing lo.hi, hi.lo, hi.hi
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[c], acc[c], 0, 0, 0);
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl[c], acc[c], 0, 0, 0);
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[c], acc[c], 0, 0, 0);
+            }
+        }
+        if (ck + kKC >= nk) {             // the batch's last chunk: its update, in order
+            const float c1 = a.bt[ct].c1, c2 = a.bt[ct].c2;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    pold[c][r] = to_storage<kDropBits>(fmaf(c2, acc[c][r], c1 * pold[c][r]));
+                acc[c] = f16v{};
+            }
+        }
+        next(ct, ck);
+    }
+    if (!live) return;
+
+    // ---- epilogue: the elements of silent blocks, unconditional buffer stores ---------------
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const bool jok = j00 + 32 * c + jl < n_out;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const uint32_t off = o0 + (uint32_t)((8 * (r >> 2) + (r & 3)) * n_out + 32 * c) * 4u;
+            const bool keep = jok && !((act_bits[c] >> il) & 1u);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pold[c][r]), rp,
+                                                  keep ? off : kDrop, 0, 0);
+        }
+    }
+}
+
 // Active blocks: one workgroup per (hidden HCU, 32 of its active input units, 4 column blocks
 // of the HCU), one wave per 32 x 32 block; workgroups past n_work store the marginal traces and
 // bias of every unit instead.
@@ -378,6 +593,20 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
     if (a.n_batches < 1 || a.n_batches > kMaxSweepBatches) return hipErrorInvalidValue;
     const int64_t n_rb = (g.n_in + 31) / 32, n_cb = (g.n_out + 31) / 32;
     const int64_t n_cg = (n_cb + kWaves - 1) / kWaves;
+    if (resident_wgs < 0) {
+        // large layer: 128 x 128 tiles, operands staged through LDS
+        void (*kernel)(Geometry, SweepArgs, int) = nullptr;
+        switch (a.drop_bits) {
+            case 0: kernel = trace_sweep_tile_kernel<0, kTileKC, kTileStages>; break;
+            case 13: kernel = trace_sweep_tile_kernel<13, kTileKC, kTileStages>; break;
+            case 16: kernel = trace_sweep_tile_kernel<16, kTileKC, kTileStages>; break;
+            default: return hipErrorInvalidValue;
+        }
+        const int64_t n_ti = (n_rb + 3) / 4;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_cg)), dim3(kWaves * 64), 0, stream,
+                              start, stop, 0, g, a, (int)n_cg);
+        return hipGetLastError();
+    }
     void (*kernel)(Geometry, SweepArgs, int, int) = nullptr;
     switch (a.drop_bits) {
         case 0: kernel = trace_sweep_kernel<0>; break;
