@@ -50,7 +50,7 @@ struct SupportLayout {
     int n_tiles, mpad, n_row_tiles;
     int kc;                        // units per chunk (multiple of 4)
     int k_alloc;                   // LDS entries of the unit table (>= the largest K_h)
-    int xstride;                   // LDS row stride of the input panel (kc + 1: no bank aliasing)
+    int xstride;                   // LDS row stride of the input panel (2 mod 32, see below)
     bool fits;                     // every thread's share of a chunk fits its staging slots
 };
 
@@ -386,7 +386,10 @@ constexpr size_t kLdsLimit = 160 * 1024;   // LDS of one gfx950 workgroup
 SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) {
     SupportLayout L;
     L.n_tiles = (g.out_mcu + 15) / 16;
-    L.mpad = L.n_tiles * 16;
+    // LDS row strides chosen so that the matrix-core operand reads of one half-wave (32 lanes:
+    // 16 rows or columns at two consecutive k) fall on 32 distinct banks: the weight rows at a
+    // stride of 16 mod 32 words, the input panel rows at 2 mod 32.
+    L.mpad = L.n_tiles * 16 + (L.n_tiles % 2 == 0 ? 16 : 0);
     L.n_row_tiles = (B + kRows - 1) / kRows;
     L.k_alloc = max_k > 0 ? max_k : 1;
     // chunk rows such that every thread holds at most `slots` weight vectors
@@ -407,7 +410,7 @@ SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) 
     // every thread must hold its share of a chunk: ceil(kc / 16) rows x vec_per_row vectors
     while (kc > 4 && ((kc + kRowGroups - 1) / kRowGroups) * vec_per_row > slots) kc -= 4;
     L.kc = kc;
-    L.xstride = L.kc + 1;
+    L.xstride = ((L.kc + 31) & ~31) + 2;
     L.fits = ((kc + kRowGroups - 1) / kRowGroups) * vec_per_row <= slots;
     return L;
 }

@@ -272,20 +272,18 @@ __device__ __forceinline__ uint32_t block_mask_bits(const Geometry& g, const uin
 }
 
 // Silent sweep of a large layer: one 128 x 128 tile (4 x 4 blocks) per workgroup of four waves,
-// wave w on row block w of the tile and all four column blocks (64 accumulators).  Per k-step
-// the workgroup needs 16 KiB of operands (x of four row blocks, t of four column blocks, hi and
-// lo); each 1 KiB fragment chunk is copied straight into LDS by the memory unit
-// (global_load_lds, 16 bytes per lane) into one of kStages stage buffers of kKC k-steps, so
-// kStages - 1 chunks are in flight while one feeds the matrix cores, with one barrier per
+// wave w on row block w of the tile and all four column blocks (64 accumulators).  The t
+// fragments of the four column blocks, which every wave reads, are copied straight into LDS by
+// the memory unit (global_load_lds, 16 bytes per lane, 1 KiB per fragment chunk) into one of
+// two stage buffers of kKC k-steps; each wave's x fragments (its own row block, read by no other
+// wave) go straight into registers; both one chunk ahead of the matrix cores, one barrier per
 // chunk.  The chunk sequence runs over all the queued batches; after a batch's last chunk the
 // wave applies that batch's update to its Pij values in registers.  Operand traffic from L2 is
 // 16 bytes per element per batch of 256 (40 with one wave per block); every wave takes part in
 // every barrier (waves past the layer compute on clamped data and store nothing).
-// Measured on the STL-shaped layer (4 batches per launch): two stages of two k-steps 3.57 ms,
-// four of one 3.74 ms, three of two (one workgroup per CU) 6.85 ms; the one-wave-per-block
-// sweep 5.21 ms.
-constexpr int kTileKC = 2;
-constexpr int kTileStages = 2;
+// Measured on the STL-shaped layer (4 batches per launch): 3.44-3.52 ms; x through LDS as well
+// 3.57-3.62 ms (deeper stages: four of one k-step 3.74 ms, three of two at one workgroup per CU
+// 6.85 ms); the one-wave-per-block sweep 5.21 ms.
 __device__ __forceinline__ void stage_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_barrier();
@@ -295,14 +293,14 @@ __device__ __forceinline__ void stage_barrier() {
 // s_waitcnt immediate with vmcnt = n (6 bits) and the other counters left alone.
 constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
-template <int kDropBits, int kKC, int kStages>
+constexpr int kTileKC = 2;
+
+template <int kDropBits, int kKC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
-    constexpr int kItems = 16 * kKC;                // 1 KiB items per chunk
+    constexpr int kItems = 8 * kKC;                 // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kWaves;
-    __shared__ u32x4 stage[kStages][kItems][64];
-    // the wave index is uniform: make that visible, so the buffer resources built from it
-    // stay in scalar registers
+    __shared__ u32x4 stage[2][kItems][64];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
@@ -318,9 +316,9 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     const int tj = in_sweep / here;
     const int n_ks = a.n_ks;
 
-    // ---- requests that do not depend on the contraction (issued first) ----------------------
     const int bi = 4 * ti + wave;
-    const int i0 = (bi < n_rb ? bi : n_rb - 1) * 32;
+    const int bic = bi < n_rb ? bi : n_rb - 1;
+    const int i0 = bic * 32;
     const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
     const bool live = bi < n_rb;                           // wave-uniform
     const int j00 = 4 * tj * 32;
@@ -343,26 +341,32 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
                                       lane);
     }
 
-    // chunk sequence over the queued batches
     int n_ch = 0;
     for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
-    // DMA of the chunk at (batch t, first k-step k0) into stage buffer sb: wave w issues items
-    // w, w + 4, ...; item = (k-step in chunk * 8 + operand block) * 2 + {hi, lo}, operand blocks
-    // 0..3 the tile's row blocks (x), 4..7 its column blocks (t)
-    auto dma = [&](int t, int k0, int sb) {
+    // requests of the chunk at (batch t, first k-step k0): the t items into stage buffer sb
+    // (item = (k-step in chunk * 4 + column block) * 2 + {hi, lo}, wave w issuing w, w + 4, ...)
+    // and this wave's x fragments into xn
+    u32x4 xc[kKC][2], xn[kKC][2];
+    auto request = [&](int t, int k0, int sb) {
         const SweepBatch bt = a.bt[t];
 #pragma unroll
         for (int q = 0; q < kPerWave; ++q) {
             const int item = wave + kWaves * q;
-            const int half = item & 1, ob = (item >> 1) & 7, kq = item >> 4;
-            int blk = ob < 4 ? 4 * ti + ob : 4 * tj + ob - 4;
-            const int nb = ob < 4 ? n_rb : n_cb;
-            blk = blk < nb ? blk : nb - 1;
+            const int half = item & 1, cb = (item >> 1) & 3, kq = item >> 3;
+            int blk = 4 * tj + cb;
+            blk = blk < n_cb ? blk : n_cb - 1;
             const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
-            const uint16_t* base = ob < 4 ? (half ? bt.x_lo : bt.x_hi) : (half ? bt.t_lo : bt.t_hi);
-            const uint16_t* src = base + (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
+            const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
+                                  (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
             __builtin_amdgcn_global_load_lds((const void*)src,
                 (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+        }
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const int64_t fa = (((int64_t)bic * n_ks + ks) * 64 + lane) * 8;
+            xn[kq][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa);
+            xn[kq][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa);
         }
     };
     auto next = [&](int& t, int& k0) {
@@ -370,48 +374,41 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
         if (k0 >= a.bt[t].nk) { k0 = 0; ++t; }
     };
 
-    // prologue: the first kStages - 1 chunks in flight
-    int dt = 0, dk = 0;                 // next chunk to request
-#pragma unroll
-    for (int q = 0; q < kStages - 1; ++q)
-        if (q < n_ch) {
-            dma(dt, dk, q);
-            next(dt, dk);
-        }
+    int dt = 0, dk = 0;
+    request(dt, dk, 0);
+    next(dt, dk);
 
     f16v acc[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] = f16v{};
-    int ct = 0, ck = 0;                 // chunk being computed
+    int ct = 0, ck = 0;
     for (int lc = 0; lc < n_ch; ++lc) {
-        // this wave's requests for chunk lc are done once at most those of the later chunks in
-        // flight remain (requests complete in order); the barrier then makes chunk lc visible
-        // to every wave and tells that every wave has finished chunk lc - 1, whose buffer is
-        // refilled below
-        const int later = n_ch - 1 - lc < kStages - 2 ? n_ch - 1 - lc : kStages - 2;
-        if (later >= kStages - 2) __builtin_amdgcn_s_waitcnt(vm_wait((kStages - 2) * kPerWave));
-        else if (later == 2) __builtin_amdgcn_s_waitcnt(vm_wait(2 * kPerWave));
-        else if (later == 1) __builtin_amdgcn_s_waitcnt(vm_wait(kPerWave));
-        else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
+        // items visible to every wave and tells that every wave is done with the other buffer
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            xc[kq][0] = xn[kq][0];
+            xc[kq][1] = xn[kq][1];
+        }
         stage_barrier();
-        if (lc + kStages - 1 < n_ch) {
-            dma(dt, dk, (lc + kStages - 1) % kStages);
+        if (lc + 1 < n_ch) {
+            request(dt, dk, (lc + 1) & 1);
             next(dt, dk);
         }
-        const int sb = lc % kStages;
+        const int sb = lc & 1;
         const int nk = a.bt[ct].nk;
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
             if (ck + kq < nk) {
-                const bf8 ah = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + wave) * 2][lane]);
-                const bf8 al = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + wave) * 2 + 1][lane]);
+                const bf8 ah = __builtin_bit_cast(bf8, xc[kq][0]);
+                const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
                 bf8 bh[4], bl[4];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + 4 + c) * 2][lane]);
-                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 8 + 4 + c) * 2 + 1][lane]);
+                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 4 + c) * 2][lane]);
+                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 4 + c) * 2 + 1][lane]);
                 }
-                // the four accumulators interleaved, each still summing lo.hi, hi.lo, hi.hi
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[c], acc[c], 0, 0, 0);
@@ -423,7 +420,7 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[c], acc[c], 0, 0, 0);
             }
         }
-        if (ck + kKC >= nk) {             // the batch's last chunk: its update, in order
+        if (ck + kKC >= nk) {
             const float c1 = a.bt[ct].c1, c2 = a.bt[ct].c2;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
@@ -436,8 +433,6 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
         next(ct, ck);
     }
     if (!live) return;
-
-    // ---- epilogue: the elements of silent blocks, unconditional buffer stores ---------------
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const bool jok = j00 + 32 * c + jl < n_out;
@@ -597,9 +592,9 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
         // large layer: 128 x 128 tiles, operands staged through LDS
         void (*kernel)(Geometry, SweepArgs, int) = nullptr;
         switch (a.drop_bits) {
-            case 0: kernel = trace_sweep_tile_kernel<0, kTileKC, kTileStages>; break;
-            case 13: kernel = trace_sweep_tile_kernel<13, kTileKC, kTileStages>; break;
-            case 16: kernel = trace_sweep_tile_kernel<16, kTileKC, kTileStages>; break;
+            case 0: kernel = trace_sweep_tile_kernel<0, kTileKC>; break;
+            case 13: kernel = trace_sweep_tile_kernel<13, kTileKC>; break;
+            case 16: kernel = trace_sweep_tile_kernel<16, kTileKC>; break;
             default: return hipErrorInvalidValue;
         }
         const int64_t n_ti = (n_rb + 3) / 4;

@@ -122,3 +122,23 @@ def test_state_calls_between_batches_see_every_update():
             tmp.train_batch(x)
         tmp.close()
     torch.cuda.synchronize()
+
+
+def test_tiled_sweep_on_a_ragged_large_layer():
+    """A layer just past the size at which the library sweeps silent blocks in 128 x 128
+    workgroup tiles (131 x 129 blocks of 32: ragged row and column tiles), five target-clamped
+    batches of mixed size (one sweep of four, one pending), against the oracle."""
+    from pairs import gpu_config
+    in_hcu, out_hcu, out_mcu = 2085, 41, 100
+    rng = np.random.default_rng(11)
+    mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0] for c in range(out_hcu)], 1)
+    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05), mask)
+    for B in (64, 64, 40, 64, 23):
+        p = rng.random((B, in_hcu)).astype(np.float32)
+        x = synth.encode_pixels(p)
+        win = rng.integers(0, out_mcu, size=(B, out_hcu))
+        target = np.zeros((B, out_hcu, out_mcu), np.float32)
+        np.put_along_axis(target, win[..., None], 1.0, axis=-1)
+        pair.train(x, target.reshape(B, -1))
+    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="tiled sweep")
+    pair.close()
