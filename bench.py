@@ -12,8 +12,10 @@ then exactly K steps are timed between two device synchronisations.
 
 Printed: one JSON line with the throughput (training samples/s), the roofline position of
 the dominant kernel (the sweep over the silent elements of Pij, timed over the timed steps with
-HIP events that its own dispatches stamp on the layer's side stream, on every 16th launch) and
-the CPU oracle's throughput on a bounded sample of the same schedule on this host.
+HIP events that its own dispatches stamp on the layer's side stream, on every 32nd launch), the
+fp64 matrix-core fraction of the support GEMM and the per-batch time of the caller's stream
+(support and active-block kernels, timed the same way), and the CPU oracle's throughput on a
+bounded sample of the same schedule on this host.
 """
 from __future__ import annotations
 
@@ -31,9 +33,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "train samples/s, MNIST-shaped 30x100 BCPNN layer; % MFMA peak, HBM GB/s"
 PEAK_HBM_GBS = 8000.0
-# Every PROFILE_PERIOD-th sweep launch of the timed steps carries dispatch-stamped events; a
-# timed launch costs the stream a few microseconds, so sampling keeps the throughput honest.
-PROFILE_PERIOD = 16
+PEAK_F64_MFMA_TFS = 78.6
+# Every PROFILE_PERIOD-th launch of each train_batch kernel in the timed steps carries
+# dispatch-stamped events; a timed launch costs its stream a few microseconds, so sampling keeps
+# the throughput honest.
+PROFILE_PERIOD = 32
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 4
 
@@ -165,7 +169,7 @@ def main():
 
     layer.profile_read()                          # applies pending sweeps; discards old timings
     # every PROFILE_PERIOD-th sweep of a long run, every sweep of a short one
-    layer.profile_enable(PROFILE_PERIOD if args.steps >= 64 * PROFILE_PERIOD else 1)
+    layer.profile_enable(PROFILE_PERIOD if args.steps >= 32 * PROFILE_PERIOD else 1)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -177,6 +181,8 @@ def main():
     torch.cuda.synchronize()
     t_end = time.perf_counter()
     sweep_ms, sweep_launches = layer.profile_read()
+    sup_ms, sup_n = layer.profile_read_kernel("support")
+    act_ms, act_n = layer.profile_read_kernel("active")
     layer.profile_enable(0)
 
     wall_s = t_end - t_start
@@ -220,10 +226,30 @@ def main():
                   "workgroup per CU, for a small layer, trace_sweep_tile_kernel, 128x128 "
                   "LDS-staged tiles, for a large one)",
         "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_launches,
-        "timed_every": PROFILE_PERIOD if args.steps >= 64 * PROFILE_PERIOD else 1,
+        "timed_every": PROFILE_PERIOD if args.steps >= 32 * PROFILE_PERIOD else 1,
         "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
         "contraction_tflops": round(flops_per_launch / avg_sweep_s / 1e12, 3),
+    }
+
+    # ---- the support GEMM on the fp64 matrix cores, and the caller's stream per batch --------
+    # Algorithmic flops of the masked support: 2 B A N_out, A = active input units per hidden
+    # HCU; both kernels are timed by their own dispatch events on the caller's stream.
+    avg_sup_s = sup_ms / 1e3 / max(sup_n, 1)
+    sup_flops = 2.0 * avg_b * k_act * L.in_mcu * L.n_out
+    mfma = {
+        "kernel": "support_kernel (masked support on fp64 MFMA, per-HCU softmax, split operands)",
+        "dtype": "f64", "achieved": round(sup_flops / avg_sup_s / 1e12, 3) if sup_n else None,
+        "peak": PEAK_F64_MFMA_TFS, "unit": "TFLOP/s",
+        "frac": round(sup_flops / avg_sup_s / 1e12 / PEAK_F64_MFMA_TFS, 4) if sup_n else None,
+        "algorithmic_flops_per_launch": sup_flops, "avg_us": round(avg_sup_s * 1e6, 3),
+        "timed_launches": sup_n,
+    }
+    critical_path = {
+        "stream": "caller's: support then active-block trace kernel, every batch",
+        "support_us": round(avg_sup_s * 1e6, 3),
+        "active_us": round(act_ms / 1e3 / max(act_n, 1) * 1e6, 3),
+        "batch_us": round(wall_s * 1e6 / args.steps, 3),
     }
 
     out = {
@@ -242,6 +268,8 @@ def main():
             "parallelism": "single GPU",
         },
         "roofline": roofline,
+        "mfma": mfma,
+        "critical_path": critical_path,
     }
 
     if not args.no_cpu_baseline and args.cpu_seconds > 0:

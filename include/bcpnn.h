@@ -169,6 +169,18 @@ bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
 bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
 
+/* The same for one kernel of train_batch: the silent-block sweep, the support (with softmax and
+ * the contraction operands) or the active-block trace kernel.  profile_enable's period applies
+ * to each kernel's own launch count.  Reads and clears that kernel's record only.  Errors:
+ * EINVAL for an unknown kernel or NULL outputs. */
+typedef enum {
+    BCPNN_KERNEL_SWEEP = 0,
+    BCPNN_KERNEL_SUPPORT = 1,
+    BCPNN_KERNEL_ACTIVE = 2
+} bcpnn_kernel;
+bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer *layer, int32_t kernel, double *total_ms,
+                                       int32_t *launches);
+
 /* Message of the calling thread's last failure ("" if none). */
 const char *bcpnn_last_error(void);
 

@@ -21,6 +21,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbcpnn.so")
 
 STORAGE = {"f32": 0, "bf16": 1, "m10": 2}
+KERNELS = {"sweep": 0, "support": 1, "active": 2}
 STATUS = {0: "BCPNN_OK", -1: "BCPNN_EINVAL", -2: "BCPNN_ENOMEM", -3: "BCPNN_EDEVICE",
           -4: "BCPNN_ESTATE"}
 
@@ -28,7 +29,7 @@ EXPORTS = [
     "bcpnn_config_default", "bcpnn_layer_create", "bcpnn_layer_destroy", "bcpnn_forward",
     "bcpnn_train_batch", "bcpnn_recompute_weights", "bcpnn_structural_update", "bcpnn_readout",
     "bcpnn_get_state", "bcpnn_set_state", "bcpnn_get_mi", "bcpnn_profile_enable",
-    "bcpnn_profile_read", "bcpnn_last_error",
+    "bcpnn_profile_read", "bcpnn_profile_read_kernel", "bcpnn_last_error",
 ]
 
 
@@ -76,6 +77,8 @@ def _load() -> ctypes.CDLL:
         "bcpnn_get_mi": (i32, [vp, vp]),
         "bcpnn_profile_enable": (i32, [vp, i32]),
         "bcpnn_profile_read": (i32, [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]),
+        "bcpnn_profile_read_kernel": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(i32)]),
         "bcpnn_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -232,12 +235,22 @@ class Layer:
 
     # -- measurement -----------------------------------------------------------------------
     def profile_enable(self, period: int = 1):
-        """Time every period-th joint-trace launch with dispatch-stamped events (0 = off)."""
+        """Time every period-th launch of each train_batch kernel with dispatch-stamped events
+        (0 = off)."""
         _check(lib.bcpnn_profile_enable(self._h, int(period)))
 
     def profile_read(self):
-        """(total ms, launches) of the joint-trace kernel since the last read."""
+        """(total ms, launches) of the silent-block sweep (the active-block kernel when the mask
+        has no silent block) since the last read."""
         ms = ctypes.c_double()
         n = ctypes.c_int32()
         _check(lib.bcpnn_profile_read(self._h, ctypes.byref(ms), ctypes.byref(n)))
+        return float(ms.value), int(n.value)
+
+    def profile_read_kernel(self, kernel: str):
+        """(total ms, launches) of one train_batch kernel ("sweep", "support", "active")."""
+        ms = ctypes.c_double()
+        n = ctypes.c_int32()
+        _check(lib.bcpnn_profile_read_kernel(self._h, KERNELS[kernel], ctypes.byref(ms),
+                                             ctypes.byref(n)))
         return float(ms.value), int(n.value)

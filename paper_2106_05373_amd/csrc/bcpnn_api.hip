@@ -74,10 +74,13 @@ struct bcpnn_layer {
     int64_t sweep_wgs = 0;               // sweep launch: one workgroup per CU, or -1 (tiles)
     bool mi_valid = false;
     bool failed = false;
-    int32_t profile_every = 0;           // 0: off; n: every n-th sweep launch carries events
-    int64_t trace_launches = 0;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
-    size_t events_used = 0;
+    int32_t profile_every = 0;           // 0: off; n: every n-th launch of a kernel carries events
+    struct KernelTimer {                 // dispatch-stamped event pairs of one kernel
+        std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+        size_t used = 0;
+        int64_t launches = 0;
+    };
+    KernelTimer timers[3];               // indexed by bcpnn_kernel
 };
 
 #define HIP_TRY(layer, expr)                                                             \
@@ -165,11 +168,34 @@ void free_layer(bcpnn_layer* L) {
     }
     if (L->sweep_ready) (void)hipEventDestroy(L->sweep_ready);
     if (L->side) (void)hipStreamDestroy(L->side);
-    for (auto& ev : L->events) {
-        (void)hipEventDestroy(ev.first);
-        (void)hipEventDestroy(ev.second);
-    }
+    for (auto& tm : L->timers)
+        for (auto& ev : tm.events) {
+            (void)hipEventDestroy(ev.first);
+            (void)hipEventDestroy(ev.second);
+        }
     delete L;
+}
+
+// Event pair for this launch of kernel k when profiling selects it (every profile_every-th
+// launch), else nulls.
+hipError_t timer_events(bcpnn_layer* L, int k, hipEvent_t* start, hipEvent_t* stop) {
+    *start = *stop = nullptr;
+    bcpnn_layer::KernelTimer& tm = L->timers[k];
+    if (L->profile_every <= 0 || tm.launches++ % L->profile_every != 0) return hipSuccess;
+    if (tm.used == tm.events.size()) {
+        std::pair<hipEvent_t, hipEvent_t> p{nullptr, nullptr};
+        hipError_t e = hipEventCreate(&p.first);
+        if (e == hipSuccess) e = hipEventCreate(&p.second);
+        if (e != hipSuccess) {
+            if (p.first) (void)hipEventDestroy(p.first);
+            return e;
+        }
+        tm.events.push_back(p);
+    }
+    *start = tm.events[tm.used].first;
+    *stop = tm.events[tm.used].second;
+    ++tm.used;
+    return hipSuccess;
 }
 
 // Enqueues the silent-element sweep of the pending batches on the side stream, after the
@@ -187,25 +213,15 @@ hipError_t launch_pending_sweep(bcpnn_layer* L) {
     a.pij = L->pij;
     a.mask = L->mask;
     a.drop_bits = L->drop_bits;
-    std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
-    hipError_t e = hipSuccess;
-    if (L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
-        if (L->events_used == L->events.size()) {
-            std::pair<hipEvent_t, hipEvent_t> p{nullptr, nullptr};
-            e = hipEventCreate(&p.first);
-            if (e == hipSuccess) e = hipEventCreate(&p.second);
-            if (e != hipSuccess) return e;
-            L->events.push_back(p);
-        }
-        ev = &L->events[L->events_used++];
-    }
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    hipError_t e = timer_events(L, BCPNN_KERNEL_SWEEP, &t0, &t1);
+    if (e != hipSuccess) return e;
     const int64_t seq = L->n_sweeps++;
     const int slot = (int)(seq % kSets);
     e = hipEventRecord(L->sweep_ready, L->stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->sweep_ready, 0);
     if (e == hipSuccess)
-        e = bcpnn::launch_trace_sweep(L->side, L->g, a, L->sweep_wgs, ev ? ev->first : nullptr,
-                                      ev ? ev->second : nullptr);
+        e = bcpnn::launch_trace_sweep(L->side, L->g, a, L->sweep_wgs, t0, t1);
     if (e == hipSuccess) e = hipEventRecord(L->sweep_done[slot], L->side);
     if (e != hipSuccess) return e;
     for (int t = 0; t < L->n_pend; ++t) L->set_sweep[L->pend[t].set] = seq;
@@ -427,9 +443,11 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     // the operand set is free once the sweep that read it last has run
     if (L->set_sweep[set] >= 0) HIP_TRY(L, wait_sweep(L, L->set_sweep[set]));
     L->set_sweep[set] = -1;
+    hipEvent_t s0, s1;
+    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_SUPPORT, &s0, &s1));
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 0, y, nullptr,
-                                     nullptr, target_dev, &L->ops[set]));
+                                     nullptr, target_dev, &L->ops[set], s0, s1));
     const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
     bcpnn::TraceArgs a;
     a.ops = L->ops[set];
@@ -449,16 +467,6 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     a.eps = L->cfg.eps;
     a.bias_gain = L->cfg.bias_gain;
     a.drop_bits = L->drop_bits;
-    std::pair<hipEvent_t, hipEvent_t>* ev = nullptr;
-    if (L->full_mask && L->profile_every > 0 && L->trace_launches++ % L->profile_every == 0) {
-        if (L->events_used == L->events.size()) {
-            std::pair<hipEvent_t, hipEvent_t> p;
-            HIP_TRY(L, hipEventCreate(&p.first));
-            HIP_TRY(L, hipEventCreate(&p.second));
-            L->events.push_back(p);
-        }
-        ev = &L->events[L->events_used++];
-    }
     if (!L->full_mask) {
         // The silent elements: swept once per kMaxSweepBatches batches on the side stream,
         // which needs only the operands (written above) and touches no element the active
@@ -466,9 +474,10 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
         L->pend[L->n_pend++] = bcpnn_layer::Pending{set, B, a.c1, a.c2};
         if (L->n_pend == bcpnn::kMaxSweepBatches) HIP_TRY(L, launch_pending_sweep(L));
     }
+    hipEvent_t a0, a1;
+    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_ACTIVE, &a0, &a1));
     HIP_TRY(L, bcpnn::launch_trace_active(L->stream, L->g, a, L->act_list, L->act_count,
-                                          L->max_active, ev ? ev->first : nullptr,
-                                          ev ? ev->second : nullptr));
+                                          L->max_active, a0, a1));
     L->cur = 1 - L->cur;
     L->ops_cur = (set + 1) % kSets;
     return BCPNN_OK;
@@ -588,25 +597,35 @@ bcpnn_status bcpnn_profile_enable(bcpnn_layer* L, int32_t enable) {
     if (bcpnn_status st = usable(L)) return st;
     if (enable < 0) return fail(BCPNN_EINVAL, "profile period must be >= 0");
     L->profile_every = enable;
-    L->trace_launches = 0;
+    for (auto& tm : L->timers) tm.launches = 0;
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer* L, int32_t kernel, double* total_ms,
+                                       int32_t* launches) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
+    if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_ACTIVE)
+        return fail(BCPNN_EINVAL, "unknown kernel %d", kernel);
+    HIP_TRY(L, join_side(L));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    bcpnn_layer::KernelTimer& tm = L->timers[kernel];
+    double sum = 0.0;
+    for (size_t k = 0; k < tm.used; ++k) {
+        float ms = 0.0f;
+        HIP_TRY(L, hipEventElapsedTime(&ms, tm.events[k].first, tm.events[k].second));
+        sum += ms;
+    }
+    *total_ms = sum;
+    *launches = (int32_t)tm.used;
+    tm.used = 0;
     return BCPNN_OK;
 }
 
 bcpnn_status bcpnn_profile_read(bcpnn_layer* L, double* total_ms, int32_t* launches) {
     if (bcpnn_status st = usable(L)) return st;
-    if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
-    HIP_TRY(L, join_side(L));
-    HIP_TRY(L, hipStreamSynchronize(L->stream));
-    double sum = 0.0;
-    for (size_t k = 0; k < L->events_used; ++k) {
-        float ms = 0.0f;
-        HIP_TRY(L, hipEventElapsedTime(&ms, L->events[k].first, L->events[k].second));
-        sum += ms;
-    }
-    *total_ms = sum;
-    *launches = (int32_t)L->events_used;
-    L->events_used = 0;
-    return BCPNN_OK;
+    return bcpnn_profile_read_kernel(L, L->full_mask ? BCPNN_KERNEL_ACTIVE : BCPNN_KERNEL_SWEEP,
+                                     total_ms, launches);
 }
 
 }  // extern "C"

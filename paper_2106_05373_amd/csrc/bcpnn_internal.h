@@ -71,7 +71,8 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
                           float* y, float* s, int32_t* winner, const float* target,
-                          const TraceOperands* ops);
+                          const TraceOperands* ops, hipEvent_t start = nullptr,
+                          hipEvent_t stop = nullptr);
 
 // Largest number of active input units (active HCUs * in_mcu) of one hidden HCU that the
 // support kernel keeps in its LDS unit table.

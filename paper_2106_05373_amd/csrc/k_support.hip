@@ -23,6 +23,8 @@
 //
 // MFMA f64 16x16x4 lane layout (verified on gfx950): A[i][k] from lane i + 16 k, B[k][j] from
 // lane j + 16 k, and lane l holds D[l / 16 + 4 r][l % 16] in result register r.
+#include <hip/hip_ext.h>
+
 #include <mutex>
 
 #include "bcpnn_internal.h"
@@ -429,7 +431,7 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
                           float* y, float* s, int32_t* winner, const float* target,
-                          const TraceOperands* ops) {
+                          const TraceOperands* ops, hipEvent_t start, hipEvent_t stop) {
     const int vec = (g.out_mcu % 4 == 0 && g.n_out % 4 == 0) ? 4 : 1;
     const SupportLayout lay = make_layout(g, B, max_active * g.in_mcu, vec);
     if (!lay.fits) return hipErrorInvalidValue;
@@ -453,9 +455,10 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     });
     auto go = [&](auto kernel) {
         const TraceOperands o = ops ? *ops : TraceOperands{};
-        kernel<<<(unsigned)blocks, kThreads, lds, stream>>>(g, lay, x, B, w, bias, act_list,
-                                                            act_count, gain, mode, y, s, winner,
-                                                            target, o, ops ? 1 : 0);
+        // the events (when given) are stamped by the dispatch itself
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, start,
+                              stop, 0, g, lay, x, B, w, bias, act_list, act_count, gain, mode, y,
+                              s, winner, target, o, ops ? 1 : 0);
         return hipGetLastError();
     };
     if (vec == 4) {

@@ -142,3 +142,28 @@ def test_tiled_sweep_on_a_ragged_large_layer():
         pair.train(x, target.reshape(B, -1))
     assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="tiled sweep")
     pair.close()
+
+
+def test_profile_records_each_kernel():
+    """Dispatch-stamped timing of each train_batch kernel: with period 1, five batches give five
+    support and five active-block launches and two sweeps (four batches, then the one the read
+    applies); an unknown kernel is rejected."""
+    import torch
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:5]]
+    lay = bcpnn().Layer(workload_config(MNIST), workload_mask(MNIST))
+    lay.profile_enable(1)
+    for x in xs:
+        lay.train_batch(x)
+    ms_sw, n_sw = lay.profile_read_kernel("sweep")
+    ms_su, n_su = lay.profile_read_kernel("support")
+    ms_ac, n_ac = lay.profile_read_kernel("active")
+    assert (n_sw, n_su, n_ac) == (2, 5, 5)
+    assert ms_sw > 0 and ms_su > 0 and ms_ac > 0
+    assert lay.profile_read_kernel("support") == (0.0, 0)          # reading clears
+    B = bcpnn()
+    import ctypes
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    st = B.lib.bcpnn_profile_read_kernel(lay._h, 7, ctypes.byref(ms), ctypes.byref(n))
+    assert st == -1, st
+    lay.profile_enable(0)
+    lay.close()
