@@ -126,10 +126,10 @@ def test_state_calls_between_batches_see_every_update():
 
 def test_tiled_sweep_on_a_ragged_large_layer():
     """A layer just past the size at which the library sweeps silent blocks in 128 x 128
-    workgroup tiles (131 x 129 blocks of 32: ragged row and column tiles), five target-clamped
+    workgroup tiles (257 x 66 blocks of 32: ragged row and column tiles), five target-clamped
     batches of mixed size (one sweep of four, one pending), against the oracle."""
     from pairs import gpu_config
-    in_hcu, out_hcu, out_mcu = 2085, 41, 100
+    in_hcu, out_hcu, out_mcu = 4100, 21, 100
     rng = np.random.default_rng(11)
     mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0] for c in range(out_hcu)], 1)
     pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05), mask)
