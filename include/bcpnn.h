@@ -110,7 +110,9 @@ void bcpnn_config_default(bcpnn_config *cfg, int32_t in_hcu, int32_t in_mcu, int
  * b = k_B log Pj, w = the masked noise described at init_noise.  mask_host is
  * [in_hcu][out_hcu] of 0/1 (NULL = every connection active); every hidden HCU needs at least
  * one active input HCU.  hip_stream is a hipStream_t (NULL = the null stream).  The layer
- * allocates about 8 * N_in * N_out bytes of device memory plus batch buffers.
+ * allocates about 8 * N_in * N_out bytes of device memory for Pij and w, 12 sets of batch
+ * operands of 4 * (N_in + N_out) * ceil(max_batch / 16) * 17 bytes each (the silent-block
+ * sweeps of queued batches read them later), and smaller buffers; it creates its second stream.
  * Errors: EINVAL (sizes, rates, mask), ENOMEM, EDEVICE. */
 bcpnn_status bcpnn_layer_create(const bcpnn_config *cfg, const uint8_t *mask_host,
                                 void *hip_stream, bcpnn_layer **out);
