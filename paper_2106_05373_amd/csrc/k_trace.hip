@@ -475,15 +475,21 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
         }
         return;
     }
+    // The x fragment pieces of the block rows (32 gathered units), the same for the four waves,
+    // are gathered once per workgroup into LDS, kActiveChunk k-steps at a time:
+    // xs[k-step][hi, lo][lane], lane = unit slot + 32 * half, exactly the A operand of a wave.
+    __shared__ u32x4 xs[kActiveChunk][2][64];
     const int lane = threadIdx.x & 63;
     const int wg = (int)xcd_linear_index(blockIdx.x, n_work);
     const int per_hcu = n_rt * n_cgr;
     const int hj = wg / per_hcu;
     const int rt = (wg - hj * per_hcu) / n_cgr;
     const int c0 = ((wg - hj * per_hcu - rt * n_cgr) * kWaves + (threadIdx.x >> 6)) * 32;
-    if (c0 >= g.out_mcu) return;                               // wave-uniform; no barriers
-    const int cols = g.out_mcu - c0 < 32 ? g.out_mcu - c0 : 32;
-    const int j0 = hj * g.out_mcu + c0;
+    // waves past the HCU's columns only help gather the x pieces (every wave takes part in
+    // every barrier); they compute on clamped columns and store nothing
+    const bool col_live = c0 < g.out_mcu;                      // wave-uniform
+    const int cols = col_live ? (g.out_mcu - c0 < 32 ? g.out_mcu - c0 : 32) : 1;
+    const int j0 = hj * g.out_mcu + (col_live ? c0 : 0);
     const int jl = lane & 31;
     const int il0 = 4 * (lane >> 5);
     const int h = lane >> 5;
@@ -506,12 +512,30 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
             opt[c][1] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb);
         }
     };
-    auto load_x = [&](int k0, int ua) {
+    // thread t gathers the pieces P = t + 256 q (unit slot P % 32 = lane % 32, half P / 32 % 2,
+    // hi / lo P / 64 % 2, k-step P / 128) of the chunk at k0; then the wave reads its operands
+    constexpr int kGather = kActiveChunk * 2 * 64 / (kWaves * 64);
+    auto gather_x = [&](int k0, int ua) {
+        u32x4 v[kGather];
+#pragma unroll
+        for (int q = 0; q < kGather; ++q) {
+            const int P = threadIdx.x + kWaves * 64 * q;
+            const int hp = (P >> 5) & 1, hl = (P >> 6) & 1, kq = P >> 7;
+            const int ks = k0 + kq < nk ? k0 + kq : nk - 1;
+            const int64_t fa = frag_chunk(ua, ks, hp, n_ks);
+            v[q] = *reinterpret_cast<const u32x4*>((hl ? a.ops.x_lo : a.ops.x_hi) + fa);
+        }
+#pragma unroll
+        for (int q = 0; q < kGather; ++q) {
+            const int P = threadIdx.x + kWaves * 64 * q;
+            xs[P >> 7][(P >> 6) & 1][P & 63] = v[q];
+        }
+    };
+    auto load_x = [&]() {
 #pragma unroll
         for (int c = 0; c < kActiveChunk; ++c) {
-            const int64_t fa = frag_chunk(ua, k0 + c < nk ? k0 + c : nk - 1, h, n_ks);
-            opx[c][0] = *reinterpret_cast<const u32x4*>(a.ops.x_hi + fa);
-            opx[c][1] = *reinterpret_cast<const u32x4*>(a.ops.x_lo + fa);
+            opx[c][0] = xs[c][0][lane];
+            opx[c][1] = xs[c][1][lane];
         }
     };
     f16v acc = {};
@@ -543,7 +567,7 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
         ur[r] = half_broadcast(ua, 8 * (r >> 2) + (r & 3), lane);
         pold[r] = a.pij[(int64_t)ur[r] * n_out + jb];
     }
-    load_x(0, ua);
+    gather_x(0, ua);
     // marginal inputs: lanes 0..31 the block's row units, 32..63 its column units
     const bool is_row = lane < 32;
     const int u = is_row ? ua : jb;
@@ -552,13 +576,19 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
     MarginalIn m;
     marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
 
-    // ---- contraction: 16-byte fragment pieces of the gathered rows and of the columns --------
+    // ---- contraction: x pieces from LDS, t pieces of the columns from memory -----------------
+    lds_barrier();
+    load_x();
     contract(0);
     for (int k0 = kActiveChunk; k0 < nk; k0 += kActiveChunk) {   // batches above 128 rows
+        lds_barrier();                                          // every wave has read its x
         load_t(k0);
-        load_x(k0, ua);
+        gather_x(k0, ua);
+        lds_barrier();
+        load_x();
         contract(k0);
     }
+    if (!col_live) return;
     const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
 
     // ---- marginal traces of the block's rows and columns, and their logs --------------------
