@@ -35,7 +35,7 @@
  *
  * Second stream: train_batch updates, on the caller's stream, everything the next batch reads
  * (Pij and w of active blocks, Pi, Pj, b, the activities).  The Pij of silent blocks are
- * updated on a stream the layer owns (default priority, non-blocking), for up to four batches
+ * updated on a stream the layer owns (default priority, non-blocking), for up to eight batches
  * in one pass with the same per-batch arithmetic; the caller's stream is made to wait for that
  * work before every call that reads or replaces Pij (get_state, set_state, structural_update,
  * recompute_weights, profile_read) and destroy waits for both streams.  The results are those
@@ -110,7 +110,7 @@ void bcpnn_config_default(bcpnn_config *cfg, int32_t in_hcu, int32_t in_mcu, int
  * b = k_B log Pj, w = the masked noise described at init_noise.  mask_host is
  * [in_hcu][out_hcu] of 0/1 (NULL = every connection active); every hidden HCU needs at least
  * one active input HCU.  hip_stream is a hipStream_t (NULL = the null stream).  The layer
- * allocates about 8 * N_in * N_out bytes of device memory for Pij and w, 12 sets of batch
+ * allocates about 8 * N_in * N_out bytes of device memory for Pij and w, 24 sets of batch
  * operands of 4 * (N_in + N_out) * ceil(max_batch / 16) * 17 bytes each (the silent-block
  * sweeps of queued batches read them later), and smaller buffers; it creates its second stream.
  * Errors: EINVAL (sizes, rates, mask), ENOMEM, EDEVICE. */

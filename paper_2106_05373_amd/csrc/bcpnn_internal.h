@@ -110,7 +110,7 @@ int64_t trace_active_workgroups(const Geometry& g, int32_t max_active);
 // takes the batches' updates Pij <- c1 Pij + c2 T in order (rounded to the storage format after
 // each, exactly as per-batch updates), and is written once.  Reads the mask; Pi, Pj, w and b
 // are untouched.  start / stop (nullable) receive the kernel's own start and end time stamps.
-constexpr int kMaxSweepBatches = 4;
+constexpr int kMaxSweepBatches = 8;
 struct SweepBatch {
     const uint16_t* x_hi;
     const uint16_t* x_lo;

@@ -3,7 +3,7 @@
 The library updates the Pij elements of active blocks every batch, and those of silent blocks
 (which the support never reads) for several consecutive batches in one sweep on a second
 stream, each batch's update applied in order with the same rounding.  Grouping must therefore
-be invisible: the state after a run is bitwise the same whether the sweeps cover four batches
+be invisible: the state after a run is bitwise the same whether the sweeps cover eight batches
 or one (reading the state applies the pending ones), and a multi-batch run without
 re-synchronisation agrees with the oracle's per-batch updates.
 """
@@ -17,8 +17,10 @@ from pairs import TOL_ACT, Pair, assert_state_close, bcpnn, max_abs, workload_co
 pytestmark = pytest.mark.gpu
 
 MNIST = synth.WORKLOADS["mnist"]
-# 11 batches of mixed sizes (a 17-row batch has a partial 16-row k-step): sweeps of 4, 4, 3
-SIZES = [128, 128, 64, 128, 128, 128, 96, 128, 128, 17, 128]
+# 20 batches of mixed sizes (a 17-row batch has a partial 16-row k-step, a 1-row batch a single
+# row): run freely, sweeps of 8 and 8 with the rest applied before a structural update or a read
+SIZES = [128, 128, 64, 128, 128, 128, 96, 128, 128, 17, 128, 128, 1, 128, 64, 128, 128, 96, 128, 128]
+STRUCTURAL_AT = 11
 
 
 @pytest.fixture(autouse=True)
@@ -38,7 +40,7 @@ def _inputs():
 
 
 def test_sweep_grouping_is_bitwise_invisible():
-    """The same batches, with a structural update before the sixth, run freely and with the
+    """The same batches, with a structural update before the twelfth, run freely and with the
     state read after every batch: bitwise identical states."""
     import torch
     xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()]
@@ -46,7 +48,7 @@ def test_sweep_grouping_is_bitwise_invisible():
     for read_each in (False, True):
         layer = bcpnn().Layer(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
         for k, x in enumerate(xs):
-            if k == 5:
+            if k == STRUCTURAL_AT:
                 layer.structural_update(count=False)
             layer.train_batch(x)
             if read_each:
@@ -59,7 +61,7 @@ def test_sweep_grouping_is_bitwise_invisible():
 
 def test_multi_batch_run_matches_oracle():
     """Target-clamped batches (the traces then depend on the inputs alone, with no feedback
-    through the weights), no re-synchronisation: after 11 batches the state agrees with the
+    through the weights), no re-synchronisation: after 20 batches the state agrees with the
     oracle to the per-step tolerances; a forward pass mid-run does not disturb the sweeps."""
     rng = np.random.default_rng(5)
     pair = Pair(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
@@ -75,7 +77,7 @@ def test_multi_batch_run_matches_oracle():
             pair.gpu.forward(pair.dev(x), y)
             _, y_o = pair.ora.forward(x)
             assert max_abs(y.cpu().numpy(), y_o) <= TOL_ACT
-    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="after 11 batches")
+    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where=f"after {len(SIZES)} batches")
     pair.close()
 
 
@@ -126,14 +128,14 @@ def test_state_calls_between_batches_see_every_update():
 
 def test_tiled_sweep_on_a_ragged_large_layer():
     """A layer just past the size at which the library sweeps silent blocks in 128 x 128
-    workgroup tiles (257 x 66 blocks of 32: ragged row and column tiles), five target-clamped
-    batches of mixed size (one sweep of four, one pending), against the oracle."""
+    workgroup tiles (257 x 66 blocks of 32: ragged row and column tiles), ten target-clamped
+    batches of mixed size (one sweep of eight, two pending), against the oracle."""
     from pairs import gpu_config
     in_hcu, out_hcu, out_mcu = 4100, 21, 100
     rng = np.random.default_rng(11)
     mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0] for c in range(out_hcu)], 1)
     pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05), mask)
-    for B in (64, 64, 40, 64, 23):
+    for B in (64, 64, 40, 64, 23, 64, 1, 64, 64, 50):
         p = rng.random((B, in_hcu)).astype(np.float32)
         x = synth.encode_pixels(p)
         win = rng.integers(0, out_mcu, size=(B, out_hcu))
@@ -145,11 +147,11 @@ def test_tiled_sweep_on_a_ragged_large_layer():
 
 
 def test_profile_records_each_kernel():
-    """Dispatch-stamped timing of each train_batch kernel: with period 1, five batches give five
-    support and five active-block launches and two sweeps (four batches, then the one the read
+    """Dispatch-stamped timing of each train_batch kernel: with period 1, nine batches give nine
+    support and nine active-block launches and two sweeps (eight batches, then the one the read
     applies); an unknown kernel is rejected."""
     import torch
-    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:5]]
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:9]]
     lay = bcpnn().Layer(workload_config(MNIST), workload_mask(MNIST))
     lay.profile_enable(1)
     for x in xs:
@@ -157,7 +159,7 @@ def test_profile_records_each_kernel():
     ms_sw, n_sw = lay.profile_read_kernel("sweep")
     ms_su, n_su = lay.profile_read_kernel("support")
     ms_ac, n_ac = lay.profile_read_kernel("active")
-    assert (n_sw, n_su, n_ac) == (2, 5, 5)
+    assert (n_sw, n_su, n_ac) == (2, 9, 9)
     assert ms_sw > 0 and ms_su > 0 and ms_ac > 0
     assert lay.profile_read_kernel("support") == (0.0, 0)          # reading clears
     B = bcpnn()
