@@ -72,7 +72,8 @@ constexpr int kChunk = 4;           // k-steps (16 batch rows each) of operands 
 constexpr int kActiveChunk = 8;     // the same in the active kernel (few waves: one round trip
                                     // covers a batch of 128)
 constexpr int kSums = 8;            // column-sum tiles requested up front (the batch for B <= 128)
-constexpr int kSweepRows = 16;      // row blocks per sweep over the column groups (see below)
+constexpr int kSweepRows = 16;      // row blocks per sweep over the column groups (tiled sweep)
+constexpr int64_t kStripeBytes = 3 << 19;  // t fragments an XCD keeps in L2 (persistent sweep)
 constexpr uint32_t kDrop = 0x80000000u;   // byte offset past every block's buffer range
 
 // Buffer resource over [p, p + bytes): raw (stride 0) addressing, 32-bit data format.  A load
@@ -132,24 +133,24 @@ __device__ __forceinline__ float marginal_value(const MarginalIn& m, const float
 // consecutive batches in order, storing the elements whose block is silent.
 template <int kDropBits>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3, 3)))
-trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work) {
+trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int stripe) {
     const int lane = threadIdx.x & 63;
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
     // Persistent: workgroup b takes work items b, b + G, ... (G = gridDim.x, a multiple of 8, so
     // they all lie on the workgroup's XCD).
     for (int item = blockIdx.x; item < n_work; item += gridDim.x) {
         // work item -> (row block, group of kWaves column blocks).  The items of one XCD form
-        // one contiguous stretch of this order, which sweeps kSweepRows row blocks over every
-        // column group, column group by column group: the x fragments of the sweep (kSweepRows
-        // blocks) stay in the XCD's L2 while the t fragments stream through it once per sweep.
+        // one contiguous stretch of this order: stripes of `stripe` column groups, each walked
+        // row block by row block.  The t fragments of a stripe (all queued batches) stay in the
+        // XCD's L2 while the x fragments of each row block are read once per stripe, by the
+        // stripe's column groups one after another.
         const int n_rb = (n_in + 31) / 32;
         const int wg = (int)xcd_linear_index(item, n_work);
-        const int sweep = wg / (kSweepRows * n_cg);
-        const int in_sweep = wg % (kSweepRows * n_cg);
-        const int rows_here = n_rb - sweep * kSweepRows < kSweepRows ? n_rb - sweep * kSweepRows
-                                                                      : kSweepRows;
-        const int bi = sweep * kSweepRows + in_sweep % rows_here;
-        const int bj = (in_sweep / rows_here) * kWaves + (threadIdx.x >> 6);
+        const int s0 = wg / (n_rb * stripe) * stripe;             // first column group
+        const int in_stripe = wg - s0 * n_rb;
+        const int groups_here = n_cg - s0 < stripe ? n_cg - s0 : stripe;
+        const int bi = in_stripe / groups_here;
+        const int bj = (s0 + in_stripe % groups_here) * kWaves + (threadIdx.x >> 6);
         const int i0 = bi * 32, j0 = bj * 32;
         if (j0 >= n_out) continue;                                 // wave-uniform; no barriers
         const int rows = n_in - i0 < 32 ? n_in - i0 : 32;
@@ -632,7 +633,7 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
                               start, stop, 0, g, a, (int)n_cg);
         return hipGetLastError();
     }
-    void (*kernel)(Geometry, SweepArgs, int, int) = nullptr;
+    void (*kernel)(Geometry, SweepArgs, int, int, int) = nullptr;
     switch (a.drop_bits) {
         case 0: kernel = trace_sweep_kernel<0>; break;
         case 13: kernel = trace_sweep_kernel<13>; break;
@@ -642,9 +643,17 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
     const int64_t n_work = n_rb * n_cg;
     int64_t grid = n_work;
     if (resident_wgs > 0 && resident_wgs < grid) grid = (resident_wgs + 7) / 8 * 8;
+    // Column groups per stripe: at most an eighth of them (one stripe or less per XCD), and few
+    // enough that the stripe's t fragments of every queued batch fit kStripeBytes.
+    int64_t ks = 0;
+    for (int t = 0; t < a.n_batches; ++t) ks += a.bt[t].nk;
+    const int64_t cg_bytes = kWaves * ks * 2 * 1024;               // hi + lo, 1 KiB per k-step
+    int64_t stripe = (n_cg + 7) / 8;
+    if (stripe * cg_bytes > kStripeBytes) stripe = kStripeBytes / cg_bytes;
+    if (stripe < 1) stripe = 1;
     // the events (when given) are stamped by the dispatch itself, so they time the kernel alone
     hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kWaves * 64), 0, stream, start,
-                          stop, 0, g, a, (int)n_cg, (int)n_work);
+                          stop, 0, g, a, (int)n_cg, (int)n_work, (int)stripe);
     return hipGetLastError();
 }
 
