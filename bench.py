@@ -40,6 +40,8 @@ PEAK_F64_MFMA_TFS = 78.6
 PROFILE_PERIOD = 32
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
+# Launches of the whole-matrix weight pass timed after the training run.
+WEIGHT_PASSES = 20
 
 # HBM traffic of the sweep kernel per launch (bytes), from rocprofv3 FETCH_SIZE and WRITE_SIZE
 # runs scaled by the copy-kernel calibration factors, keyed by workload and the SHA-256 of the
@@ -262,6 +264,26 @@ def main():
         "batch_us": round(wall_s * 1e6 / args.steps, 3),
     }
 
+    # ---- the log-weight pass over the whole matrix (recompute_weights), after the timed run ---
+    # Per launch it writes every w and reads the Pij of active blocks (a silent weight is 0
+    # whatever its trace), plus Pi, Pj and the mask.  Timed by its own dispatch events.
+    layer.profile_enable(1)
+    for _ in range(WEIGHT_PASSES):
+        layer.recompute_weights()
+    wp_ms, wp_n = layer.profile_read_kernel("weights")
+    layer.profile_enable(0)
+    wp_bytes = 4.0 * E + 4.0 * active + 4.0 * (L.n_in + L.n_out) + L.in_hcu * L.out_hcu
+    wp_s = wp_ms / 1e3 / max(wp_n, 1)
+    weight_pass = {
+        "kernel": "recompute_weights_vec_kernel (w = mask ? log(Pij / (Pi Pj)) : 0 over the "
+                  "whole matrix, Pij read for active blocks only)",
+        "bound": "hbm", "achieved": round(wp_bytes / wp_s / 1e9, 1) if wp_n else None,
+        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+        "frac": round(wp_bytes / wp_s / 1e9 / PEAK_HBM_GBS, 4) if wp_n else None,
+        "algorithmic_bytes_per_launch": wp_bytes, "avg_us": round(wp_s * 1e6, 3),
+        "timed_launches": wp_n,
+    }
+
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
@@ -280,6 +302,7 @@ def main():
         "roofline": roofline,
         "mfma": mfma,
         "critical_path": critical_path,
+        "weight_pass": weight_pass,
     }
 
     if not args.no_cpu_baseline and args.cpu_seconds > 0:

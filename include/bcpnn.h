@@ -171,14 +171,16 @@ bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
 bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
 
-/* The same for one kernel of train_batch: the silent-block sweep, the support (with softmax and
- * the contraction operands) or the active-block trace kernel.  profile_enable's period applies
- * to each kernel's own launch count.  Reads and clears that kernel's record only.  Errors:
- * EINVAL for an unknown kernel or NULL outputs. */
+/* The same for one kernel: the silent-block sweep, the support (with softmax and the
+ * contraction operands) or the active-block trace kernel of train_batch, or the weight pass of
+ * recompute_weights (w over the whole matrix; the bias kernel after it is not included).
+ * profile_enable's period applies to each kernel's own launch count.  Reads and clears that
+ * kernel's record only.  Errors: EINVAL for an unknown kernel or NULL outputs. */
 typedef enum {
     BCPNN_KERNEL_SWEEP = 0,
     BCPNN_KERNEL_SUPPORT = 1,
-    BCPNN_KERNEL_ACTIVE = 2
+    BCPNN_KERNEL_ACTIVE = 2,
+    BCPNN_KERNEL_WEIGHTS = 3
 } bcpnn_kernel;
 bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer *layer, int32_t kernel, double *total_ms,
                                        int32_t *launches);

@@ -21,7 +21,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbcpnn.so")
 
 STORAGE = {"f32": 0, "bf16": 1, "m10": 2}
-KERNELS = {"sweep": 0, "support": 1, "active": 2}
+KERNELS = {"sweep": 0, "support": 1, "active": 2, "weights": 3}
 STATUS = {0: "BCPNN_OK", -1: "BCPNN_EINVAL", -2: "BCPNN_ENOMEM", -3: "BCPNN_EDEVICE",
           -4: "BCPNN_ESTATE"}
 

@@ -80,7 +80,7 @@ struct bcpnn_layer {
         size_t used = 0;
         int64_t launches = 0;
     };
-    KernelTimer timers[3];               // indexed by bcpnn_kernel
+    KernelTimer timers[4];               // indexed by bcpnn_kernel
 };
 
 #define HIP_TRY(layer, expr)                                                             \
@@ -486,9 +486,12 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
 bcpnn_status bcpnn_recompute_weights(bcpnn_layer* L) {
     if (bcpnn_status st = usable(L)) return st;
     HIP_TRY(L, join_side(L));
+    hipEvent_t t0, t1;
+    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_WEIGHTS, &t0, &t1));
     HIP_TRY(L, bcpnn::launch_recompute_weights(L->stream, L->g, L->mask, L->pi[L->cur],
                                                L->pj[L->cur], L->pij, L->cfg.eps,
-                                               L->cfg.bias_gain, L->drop_bits, L->w, L->b));
+                                               L->cfg.bias_gain, L->drop_bits, L->w, L->b,
+                                               t0, t1));
     return BCPNN_OK;
 }
 
@@ -605,7 +608,7 @@ bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer* L, int32_t kernel, double* t
                                        int32_t* launches) {
     if (bcpnn_status st = usable(L)) return st;
     if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
-    if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_ACTIVE)
+    if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_WEIGHTS)
         return fail(BCPNN_EINVAL, "unknown kernel %d", kernel);
     HIP_TRY(L, join_side(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));

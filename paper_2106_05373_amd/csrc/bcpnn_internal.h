@@ -35,7 +35,8 @@ hipError_t launch_bias(hipStream_t stream, const Geometry& g, const float* pj, f
 hipError_t launch_recompute_weights(hipStream_t stream, const Geometry& g, const uint8_t* mask,
                                     const float* pi, const float* pj, const float* pij,
                                     float eps, float bias_gain, int drop_bits, float* w,
-                                    float* b);
+                                    float* b, hipEvent_t start = nullptr,
+                                    hipEvent_t stop = nullptr);
 
 // Zeroes the silent blocks of w (used after a host upload of w).
 hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_t* mask,

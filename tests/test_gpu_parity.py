@@ -228,6 +228,47 @@ def test_recompute_weights_matches_oracle():
     pair.close()
 
 
+@pytest.mark.parametrize("in_hcu,out_hcu,out_mcu,storage", [
+    (40, 12, 3, "f32"),     # N_out % 4 == 0, a 16-byte group spans two hidden HCUs
+    (40, 10, 2, "f32"),     # two HCUs per group
+    (40, 8, 1, "f32"),      # one MCU per HCU: the scalar kernel
+    (40, 9, 4, "f32"),      # groups aligned to the HCUs
+    (40, 7, 5, "f32"),      # N_out % 4 != 0: the scalar kernel
+    (64, 41, 100, "f32"),   # 1025 groups per row: several accesses per lane, ragged last one
+    (64, 41, 100, "bf16"),
+    (40, 12, 3, "m10"),
+])
+def test_recompute_weights_on_any_state(in_hcu, out_hcu, out_mcu, storage):
+    """The weight pass over an arbitrary state (traces not consistent with each other, some
+    below eps, a random mask): every w and b against the oracle's, silent weights exactly 0."""
+    from pairs import gpu_config
+    rng = np.random.default_rng(in_hcu * 1000 + out_hcu * 10 + out_mcu)
+    cfg = gpu_config(in_hcu, 2, out_hcu, out_mcu, 16, storage=storage)
+    mask = (rng.random((in_hcu, out_hcu)) < 0.3).astype(np.uint8)
+    mask[rng.integers(0, in_hcu, out_hcu), np.arange(out_hcu)] = 1
+    pair = Pair(cfg, mask)
+    n_in, n_out = pair.n_in, pair.n_out
+    st = pair.ora.get_state()
+    st["pi"] = rng.uniform(1e-9, 1.0, n_in).astype(np.float32)
+    st["pj"] = rng.uniform(1e-9, 0.5, n_out).astype(np.float32)
+    pij = rng.uniform(0.0, 0.3, (n_in, n_out)).astype(np.float32)
+    pij[rng.random((n_in, n_out)) < 0.05] = 1e-10                  # below eps
+    st["pij"] = pij
+    st["w"] = np.full_like(st["w"], 7.0)                             # overwritten everywhere
+    st["b"] = np.zeros_like(st["b"])
+    pair.gpu.set_state(st)
+    pair.ora.set_state(st)
+    pair.gpu.recompute_weights()
+    pair.ora.recompute_weights()
+    sg = pair.gpu.get_state()
+    from pairs import TOL_W_STORAGE
+    assert_weights_close(sg["w"], pair.ora.w, tol=TOL_W_STORAGE[storage])
+    assert_weights_close(sg["b"], pair.ora.b)
+    silent = np.repeat(np.repeat(mask == 0, 2, axis=0), out_mcu, axis=1)
+    assert np.all(sg["w"].reshape(n_in, n_out)[silent] == 0.0)
+    pair.close()
+
+
 def test_runs_are_bitwise_deterministic():
     w = MNIST
     X, _ = encoded(w, 128 * 6)
