@@ -85,6 +85,9 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
                float gain, int mode, float* __restrict__ y, float* __restrict__ s,
                int32_t* __restrict__ winner, const float* __restrict__ target,
                TraceOperands ops, int has_ops) {
+    // Highest wave priority: on a CU shared with the silent sweep (second stream), the SIMD
+    // arbiter issues this kernel's instructions first.
+    __builtin_amdgcn_s_setprio(3);
     typedef float vec_t __attribute__((ext_vector_type(kVec)));
     constexpr int kSlots = stage_slots(kTilesPerWave, kVec);
     extern __shared__ float lds[];

@@ -455,6 +455,8 @@ template <int kDropBits>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_list,
                     const int32_t* __restrict__ act_count, int n_rt, int n_cgr, int n_work) {
+    // Highest wave priority, as in the support kernel: it shares CUs with the silent sweep.
+    __builtin_amdgcn_s_setprio(3);
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
     const int nk = (a.B + 15) / 16;
     const int n_ks = a.ops.n_ks;
