@@ -75,6 +75,23 @@ __device__ __forceinline__ void write_split_column(const float (&v)[kRows], uint
     *reinterpret_cast<uint4*>(lo + c1) = make_uint4(l[4], l[5], l[6], l[7]);
 }
 
+// The same for one half (rows 8 h .. 8 h + 7) of the 16 entries: one 16-byte chunk each.
+__device__ __forceinline__ void write_split_half(const float (&v)[kRows / 2], uint16_t* hi,
+                                                 uint16_t* lo, int64_t u, int ks, int h,
+                                                 int32_t n_ks) {
+    uint32_t hh[kRows / 4], ll[kRows / 4];
+#pragma unroll
+    for (int q = 0; q < kRows / 4; ++q) {
+        const __bf16 h0 = (__bf16)v[2 * q], h1 = (__bf16)v[2 * q + 1];
+        const __bf16 l0 = (__bf16)(v[2 * q] - (float)h0), l1 = (__bf16)(v[2 * q + 1] - (float)h1);
+        hh[q] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+        ll[q] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+    }
+    const int64_t c = frag_chunk(u, ks, h, n_ks);
+    *reinterpret_cast<uint4*>(hi + c) = make_uint4(hh[0], hh[1], hh[2], hh[3]);
+    *reinterpret_cast<uint4*>(lo + c) = make_uint4(ll[0], ll[1], ll[2], ll[3]);
+}
+
 // kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
 // kVec: 4 when weight row segments can be read as float4 (M_out and N_out multiples of 4).
 template <int kTilesPerWave, int kVec>
@@ -364,20 +381,33 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     // k-step): the hidden HCU's columns of t (the activity above, or the target) and the input
     // columns [c0, c1) of x, each column split into bf16 hi / lo parts and written in fragment
     // order, plus the column sums over these rows.  Rows past B are written as zeros.
+    // The t columns go out in halves of 8 rows (one 16-byte fragment chunk of hi and of lo per
+    // half), so that 2 M_out threads share the work; the two halves of a column sit in
+    // neighbouring lanes and add their row sums with one lane exchange.
     lds_barrier();
-    for (int m = tid; m < g.out_mcu; m += kThreads) {
-        float v[kRows];
+    const int n_half = 2 * g.out_mcu;
+    for (int base = 0; base < n_half; base += kThreads) {          // uniform trip count
+        const int q = base + tid;
+        const bool live = q < n_half;
+        const int m = live ? q >> 1 : 0;
+        const int half = q & 1;
+        float v[kRows / 2];
         float sum = 0.0f;
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-            v[r] = r < rows ? (target ? target[(int64_t)(row0 + r) * g.n_out + col_base + m]
-                                      : stile[r * mpad + m])
-                            : 0.0f;
-            sum += v[r];
+        for (int i = 0; i < kRows / 2; ++i) {
+            const int r = 8 * half + i;
+            v[i] = live && r < rows
+                       ? (target ? target[(int64_t)(row0 + r) * g.n_out + col_base + m]
+                                 : stile[r * mpad + m])
+                       : 0.0f;
+            sum += v[i];
         }
-        const int64_t col = col_base + m;
-        write_split_column(v, ops.t_hi, ops.t_lo, col, rt, ops.n_ks);
-        ops.t_sum[(int64_t)rt * g.n_out + col] = sum;
+        const float total = sum + __shfl_xor(sum, 1, 64);           // same bits in both lanes
+        if (live) {
+            const int64_t col = col_base + m;
+            write_split_half(v, ops.t_hi, ops.t_lo, col, rt, half, ops.n_ks);
+            if (half == 0) ops.t_sum[(int64_t)rt * g.n_out + col] = total;
+        }
     }
     for (int p = pass0; p < n_pass; p += kWaves) {
         if (p != pass0) split_load(p);
