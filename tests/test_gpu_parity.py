@@ -344,8 +344,8 @@ def test_other_shapes_one_step(shape):
 
 def test_stl_shape_sampled():
     """The STL-shaped layer at full size (55296 x 10000 traces, 5% receptive fields, batch 256)
-    in the launch configuration the benchmark uses: one structural update and one batch, checked
-    on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
+    in the launch configuration the benchmark uses: one structural update, one batch and the
+    whole-matrix weight pass, checked on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
     from the GPU's prior weights, and the sampled blocks of the traces and weights from the
     prior state restricted to the sampled input and hidden HCUs (the trace and weight updates
     are elementwise given the batch, so a sub-problem reproduces them exactly)."""
@@ -396,6 +396,12 @@ def test_stl_shape_sampled():
     m_sub = after_swap["mask"][np.ix_(hi_s, hj_s)]
     w_o, _ = oracle.update_weights(sub["p"], m_sub, pi, pj, pij)
     assert_weights_close(sub_post["w"], w_o)
+    # the whole-matrix weight pass (one row per workgroup at this size) on the same state
+    layer.recompute_weights()
+    w_re = layer.get_state(("w",))["w"][np.ix_(sub["rows"], cols)]
+    w_ro, _ = oracle.update_weights(sub["p"], m_sub, sub_post["pi"], sub_post["pj"],
+                                    sub_post["pij"])
+    assert_weights_close(w_re, w_ro)
     layer.close()
 
 
