@@ -45,6 +45,7 @@ constexpr int stage_slots(int tiles_per_wave, int vec) {
     return vec == 4 ? (tiles_per_wave >= 4 ? 8 : 12) : (tiles_per_wave >= 8 ? 32 : 16);
 }
 constexpr int kXRegs = 8;             // input elements staged per thread per chunk
+constexpr int kLeanSlots = 8;         // weight vectors per thread in the lean variant (see launch)
 constexpr int kRowGroups = kThreads / 32;   // weight rows staged side by side (32 lanes each)
 static_assert(kRowGroups == kRows, "one row group per batch row of the input panel");
 
@@ -94,7 +95,7 @@ __device__ __forceinline__ void write_split_half(const float (&v)[kRows / 2], ui
 
 // kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
 // kVec: 4 when weight row segments can be read as float4 (M_out and N_out multiples of 4).
-template <int kTilesPerWave, int kVec>
+template <int kTilesPerWave, int kVec, int kLeanSlots = 0>
 __global__ void __launch_bounds__(kThreads)
 support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32_t B,
                const float* __restrict__ w, const float* __restrict__ bias,
@@ -106,7 +107,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     // arbiter issues this kernel's instructions first.
     __builtin_amdgcn_s_setprio(3);
     typedef float vec_t __attribute__((ext_vector_type(kVec)));
-    constexpr int kSlots = stage_slots(kTilesPerWave, kVec);
+    constexpr int kSlots = kLeanSlots > 0 ? kLeanSlots : stage_slots(kTilesPerWave, kVec);
     extern __shared__ float lds[];
     const int kc = lay.kc, mpad = lay.mpad, xstride = lay.xstride;
     int32_t* units = reinterpret_cast<int32_t*>(lds);               // [k_alloc]
@@ -418,7 +419,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
 constexpr size_t kLdsBudget = 120 * 1024;
 constexpr size_t kLdsLimit = 160 * 1024;   // LDS of one gfx950 workgroup
 
-SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) {
+SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec, int lean_slots = 0) {
     SupportLayout L;
     L.n_tiles = (g.out_mcu + 15) / 16;
     // LDS row strides chosen so that the matrix-core operand reads of one half-wave (32 lanes:
@@ -430,7 +431,10 @@ SupportLayout make_layout(const Geometry& g, int32_t B, int32_t max_k, int vec) 
     // chunk rows such that every thread holds at most `slots` weight vectors
     const int vec_per_row = (g.out_mcu / vec + 31) / 32;
     const int tpw = (L.n_tiles + kWaves - 1) / kWaves;
-    const int slots = stage_slots(tpw <= 1 ? 1 : tpw <= 2 ? 2 : tpw <= 4 ? 4 : kMaxTilesPerWave, vec);
+    const int slots = lean_slots > 0 ? lean_slots
+                                     : stage_slots(tpw <= 1 ? 1 : tpw <= 2 ? 2 : tpw <= 4 ? 4
+                                                                             : kMaxTilesPerWave,
+                                                   vec);
     const int by_regs_w = kRowGroups * (slots / vec_per_row);
     const int by_regs_x = 32 * kXRegs;
     const size_t fixed = (size_t)((L.k_alloc + 3) & ~3) * sizeof(int32_t);
@@ -466,7 +470,12 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
                           float* y, float* s, int32_t* winner, const float* target,
                           const TraceOperands* ops, hipEvent_t start, hipEvent_t stop) {
     const int vec = (g.out_mcu % 4 == 0 && g.n_out % 4 == 0) ? 4 : 1;
-    const SupportLayout lay = make_layout(g, B, max_active * g.in_mcu, vec);
+    SupportLayout lay = make_layout(g, B, max_active * g.in_mcu, vec);
+    // A layer whose active rows take several chunks anyway stages fewer weight vectors per
+    // thread (kLeanSlots): the kernel then needs few enough registers to share a SIMD with a
+    // workgroup of the tiled silent sweep, which runs beside it on large layers.
+    const bool lean = vec == 4 && lay.n_tiles <= kWaves && lay.kc < max_active * g.in_mcu;
+    if (lean) lay = make_layout(g, B, max_active * g.in_mcu, vec, kLeanSlots);
     if (!lay.fits) return hipErrorInvalidValue;
     const size_t lds = lds_bytes(lay);
     const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
@@ -475,7 +484,8 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     // variant, to the largest size a launch can ask for
     static std::once_flag raised;
     std::call_once(raised, [] {
-        const void* all[] = {(const void*)support_kernel<1, 4>, (const void*)support_kernel<2, 4>,
+        const void* all[] = {(const void*)support_kernel<1, 4, kLeanSlots>,
+                             (const void*)support_kernel<1, 4>, (const void*)support_kernel<2, 4>,
                              (const void*)support_kernel<4, 4>,
                              (const void*)support_kernel<kMaxTilesPerWave, 4>,
                              (const void*)support_kernel<1, 1>, (const void*)support_kernel<2, 1>,
@@ -495,6 +505,7 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
         return hipGetLastError();
     };
     if (vec == 4) {
+        if (lean) return go(support_kernel<1, 4, kLeanSlots>);
         if (tpw <= 1) return go(support_kernel<1, 4>);
         if (tpw <= 2) return go(support_kernel<2, 4>);
         if (tpw <= 4) return go(support_kernel<4, 4>);
