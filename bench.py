@@ -48,10 +48,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "d0114ba8719da0fb747b0ac915799cf406f15e8c4cf0fa3392ea0110b4224330"): 22010000,
+    ("mnist", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 22008730,
+    ("stl", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 2406025873,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "d0114ba8719da0fb747b0ac915799cf406f15e8c4cf0fa3392ea0110b4224330"): 121913200,
+    ("mnist", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 121059635,
+    ("stl", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 19677732193,
 }
 
 
