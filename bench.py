@@ -98,6 +98,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle baseline sample (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pairs", action="store_true",
+                    help="contract every input unit instead of exploiting the (x, 1 - x) pixel "
+                         "pairs (complement_pairs = 0)")
     ap.add_argument("--precision-report", action="store_true",
                     help="reduced-precision storage: readout-pipeline accuracy with Pij and W in "
                          "fp32 / bf16 / 10-bit mantissa, hidden code against the fp32 oracle")
@@ -151,6 +154,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     L = w.layer
     B = w.batch
+    pairs = 0 if args.no_pairs else int(w.complement_pairs)
     n_steps = args.warmup + args.steps
     sched = schedule(w.n_train, B, w.period, n_steps)
     epochs = sorted({s[0] for s in sched})
@@ -171,7 +175,8 @@ def main():
 
     stream = torch.cuda.Stream(device=dev)
     cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
-                               gain=w.gain, init_noise=w.init_noise, seed=w.seed_noise)
+                               gain=w.gain, init_noise=w.init_noise, seed=w.seed_noise,
+                               complement_pairs=pairs)
     layer = bcpnn.Layer(cfg, mask, stream=stream)
 
     def step(s):
@@ -212,11 +217,12 @@ def main():
     # ---- roofline of the dominant kernel: the silent-element sweep -------------------------
     # Per launch it must read every Pij and write those of silent blocks (4 + 4 bytes per silent
     # element, 4 per active one), and read the split operands of each batch it applies once
-    # (bf16 hi and lo of x and t, 4 bytes per element per padded batch row, plus the column
-    # sums).  Its contractions run on bf16 matrix cores (three split products per batch), whose
-    # time is a fraction of that traffic's, so the bound is HBM bandwidth.  It runs on the
-    # layer's second stream, one workgroup per CU, overlapping the next batches' support and
-    # active-block kernels, so its duration is set by that sharing as much as by its traffic.
+    # (bf16 hi and lo of x and t, 4 bytes per element per padded batch row; with complement
+    # pairs x covers the first unit of each input HCU only, and the column sums of t per
+    # 16-row tile are read as well).  Its contractions run on bf16 matrix cores (three split
+    # products per batch).  It runs on the layer's second stream, one workgroup per CU for a
+    # small layer, overlapping the next batches' support and active-block kernels, so its
+    # duration is set by that sharing as much as by its traffic.
     sizes = sweep_sizes(sched, args.warmup, n_steps)
     per_sweep = sum(sizes) / len(sizes)
     avg_b = samples / max(args.steps, 1)
@@ -224,24 +230,28 @@ def main():
     active = k_act * L.in_mcu * L.n_out
     E = L.n_in * L.n_out
     pij_bytes = 4.0 * E + 4.0 * (E - active)
-    ops_bytes = 4.0 * (L.n_in + L.n_out) * b_pad + 4.0 * (L.n_in + L.n_out) * (b_pad // 16)
+    n_x = L.in_hcu if pairs else L.n_in            # input units the contraction covers
+    ops_bytes = 4.0 * (n_x + L.n_out) * b_pad + (4.0 * L.n_out * (b_pad // 16) if pairs else 0.0)
     bytes_per_launch = pij_bytes + per_sweep * ops_bytes
     if sweep_launches == 0 or sweep_ms <= 0:
         raise RuntimeError("no sweep launch was timed")
     avg_sweep_s = sweep_ms / 1e3 / sweep_launches
     achieved_gbs = bytes_per_launch / avg_sweep_s / 1e9
-    flops_per_launch = 2.0 * E * avg_b * per_sweep
+    flops_per_launch = 2.0 * n_x * L.n_out * avg_b * per_sweep
     csrc = os.path.join(ROOT, "paper_2106_05373_amd", "csrc")
     digest = source_digest(csrc)
-    traffic = MEASURED_TRAFFIC.get((args.workload, digest))
+    traffic_key = args.workload if pairs else args.workload + ":unpaired"
+    traffic = MEASURED_TRAFFIC.get((traffic_key, digest))
     roofline = {
         "bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS,
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
         "kernel": "silent-block trace sweep (the x^T t contractions of up to "
                   f"{SWEEP_BATCHES} consecutive batches on split-bf16 MFMA, one read and one write "
-                  "of Pij; on a second stream overlapping later batches: trace_sweep_kernel, one "
-                  "workgroup per CU, for a small layer, trace_sweep_tile_kernel, 128x128 "
-                  "LDS-staged tiles, for a large one)",
+                  "of Pij; on a second stream overlapping later batches: one workgroup per CU "
+                  "for a small layer, LDS-staged tiles for a large one; "
+                  + ("trace_sweep_pair_kernel / trace_sweep_pair_tile_kernel: over the first "
+                     "unit of each (x, 1 - x) input pair, the second row from the column total)"
+                     if pairs else "trace_sweep_kernel / trace_sweep_tile_kernel)"),
         "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_launches,
         "timed_every": PROFILE_PERIOD if args.steps >= 32 * PROFILE_PERIOD else 1,
         "batches_per_launch": round(per_sweep, 3),
@@ -285,7 +295,7 @@ def main():
         "bound": "hbm", "achieved": round(wp_bytes / wp_s / 1e9, 1) if wp_n else None,
         "peak": PEAK_HBM_GBS, "unit": "GB/s",
         "frac": round(wp_bytes / wp_s / 1e9 / PEAK_HBM_GBS, 4) if wp_n else None,
-        "traffic": MEASURED_WEIGHT_TRAFFIC.get((args.workload, digest)),
+        "traffic": MEASURED_WEIGHT_TRAFFIC.get((traffic_key, digest)),
         "algorithmic_bytes_per_launch": wp_bytes, "avg_us": round(wp_s * 1e6, 3),
         "timed_launches": wp_n,
     }
@@ -302,7 +312,8 @@ def main():
                         f"{w.period} batches, alpha {w.alpha}",
             "global_batch": B, "samples_timed": samples, "structural_updates_timed": plastic_steps,
             "gpu_event_s": round(gpu_s, 6), "wall_s": round(wall_s, 6),
-            "support_accumulation": "f64", "data_staging_s": round(prep_s, 2),
+            "support_accumulation": "f64", "complement_pairs": bool(pairs),
+            "data_staging_s": round(prep_s, 2),
             "parallelism": "single GPU",
         },
         "roofline": roofline,
@@ -339,7 +350,7 @@ def run_pipeline(args):
                              w.seed_mask)
     cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
                                gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
-                               seed=w.seed_noise)
+                               seed=w.seed_noise, complement_pairs=int(w.complement_pairs))
     net = Network(cfg, mask, w.readout_mcu)
     per_epoch = (w.n_train + B - 1) // B
 
@@ -480,7 +491,8 @@ def run_precision_report(args):
 
     rows = {}
     for st in ("f32", "bf16", "m10"):
-        cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, storage=st, **kw)
+        cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, storage=st,
+                                   complement_pairs=int(w.complement_pairs), **kw)
         net = Network(cfg, mask, w.readout_mcu)
         for e in range(w.epochs + w.readout_epochs):
             perm = synth.epoch_permutation(w.n_train, w.seed_shuffle, e)

@@ -93,6 +93,15 @@ typedef struct {
     uint64_t seed;
     int32_t n_swaps;            /* swaps per hidden HCU per structural update (>= 0)          */
     int32_t storage;            /* bcpnn_storage                                              */
+    int32_t complement_pairs;   /* 0 or 1.  1 declares that every input HCU has two MCUs whose
+                                   activities are x and 1 - x (the pixel encoding of the
+                                   paper's image inputs; requires in_mcu == 2).  The batch sum
+                                   of the second row of each pair is then taken as
+                                   sum_b t_bj - sum_b x_b t_bj, equal in real arithmetic for
+                                   such inputs, so the joint-trace contraction runs over half
+                                   the input units.  Inputs that are not complementary pairs
+                                   get that update all the same.  0 (the default) contracts
+                                   every input unit.                                          */
 } bcpnn_config;
 
 /* Host-side view of the layer state (fp32 arrays and the uint8 mask, layouts above). */
@@ -102,7 +111,8 @@ typedef struct {
 } bcpnn_state_view;
 
 /* Fills cfg with the defaults (alpha 1e-3, one cycle, gain 1, k_B 1, eps 1e-8, uniform initial
- * traces, init_noise 0.1, seed 0, one swap, fp32 storage) for the given sizes. */
+ * traces, init_noise 0.1, seed 0, one swap, fp32 storage, complement_pairs 0) for the given
+ * sizes. */
 void bcpnn_config_default(bcpnn_config *cfg, int32_t in_hcu, int32_t in_mcu, int32_t out_hcu,
                           int32_t out_mcu, int32_t max_batch);
 

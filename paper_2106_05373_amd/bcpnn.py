@@ -44,6 +44,7 @@ class Config(ctypes.Structure):
         ("pi_init", ctypes.c_float), ("pj_init", ctypes.c_float),
         ("init_noise", ctypes.c_float), ("seed", ctypes.c_uint64),
         ("n_swaps", ctypes.c_int32), ("storage", ctypes.c_int32),
+        ("complement_pairs", ctypes.c_int32),
     ]
 
 

@@ -122,6 +122,9 @@ const char* check_config(const bcpnn_config* c) {
     if (c->storage != BCPNN_STORE_F32 && c->storage != BCPNN_STORE_BF16 &&
         c->storage != BCPNN_STORE_M10)
         return "unknown storage format";
+    if (c->complement_pairs != 0 && c->complement_pairs != 1)
+        return "complement_pairs must be 0 or 1";
+    if (c->complement_pairs && c->in_mcu != 2) return "complement_pairs needs in_mcu == 2";
     return nullptr;
 }
 
@@ -147,7 +150,9 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
         return "a hidden HCU has more than 12288 active input units (active HCUs * in_mcu)";
     const Geometry g{c.in_hcu, c.in_mcu, c.out_hcu, c.out_mcu, (int64_t)c.in_hcu * c.in_mcu,
                      (int64_t)c.out_hcu * c.out_mcu};
-    if (bcpnn::trace_active_workgroups(g, max_active) >= (1ll << 24))
+    // (with complement pairs, the larger of the two launch shapes)
+    const int mode = c.complement_pairs ? bcpnn::kPairsSplit : bcpnn::kUnpaired;
+    if (bcpnn::trace_active_workgroups(g, max_active, mode) >= (1ll << 24))
         return "the active-block trace launch would exceed 2^24 workgroups "
                "(out_hcu * ceil(active units / 32) * ceil(out_mcu / 128) too large)";
     return nullptr;
@@ -205,11 +210,12 @@ hipError_t launch_pending_sweep(bcpnn_layer* L) {
     bcpnn::SweepArgs a{};
     for (int t = 0; t < L->n_pend; ++t) {
         const bcpnn::TraceOperands& o = L->ops[L->pend[t].set];
-        a.bt[t] = bcpnn::SweepBatch{o.x_hi, o.x_lo, o.t_hi, o.t_lo,
+        a.bt[t] = bcpnn::SweepBatch{o.x_hi, o.x_lo, o.t_hi, o.t_lo, o.t_sum,
                                     (L->pend[t].B + 15) / 16, L->pend[t].c1, L->pend[t].c2};
     }
     a.n_batches = L->n_pend;
     a.n_ks = L->ops[0].n_ks;
+    a.paired = L->ops[0].paired;
     a.pij = L->pij;
     a.mask = L->mask;
     a.drop_bits = L->drop_bits;
@@ -370,6 +376,12 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t blocks = ((g.n_in + 31) / 32) * ((g.n_out + 31) / 32);
     if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : -1;
+    // complement pairs: a small layer's active-block kernel splits the rows of each pair over
+    // two waves (it is bound by latency, not by its matrix work)
+    const int pair_mode = !cfg->complement_pairs ? bcpnn::kUnpaired
+                          : L->sweep_wgs > 0     ? bcpnn::kPairsSplit
+                                                 : bcpnn::kPairs;
+    for (int k = 0; k < kSets; ++k) L->ops[k].paired = pair_mode;
     if (e != hipSuccess) {
         free_layer(L);
         return fail(e == hipErrorOutOfMemory ? BCPNN_ENOMEM : BCPNN_EDEVICE,

@@ -52,6 +52,9 @@ hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_
 // 16 batch rows, 64 lanes x 8 bf16 (1 KiB), lane l holding rows 8 (l / 32) .. + 7 of unit
 // l % 32 -- exactly the A / B operand of v_mfma_f32_32x32x16_bf16, so a wave loads one step of
 // one operand as a single contiguous 1 KiB read.  Units past the layer stay zero.
+// With complement pairs (every input HCU holds x and 1 - x), x^T holds the first unit of each
+// input HCU only, indexed by the HCU: [ceil(in_hcu / 32)][n_ks][64][8]; x_sum still has every
+// unit.
 struct TraceOperands {
     uint16_t* x_hi;   // [ceil(n_in / 32)][n_ks][64][8] bf16 bits
     uint16_t* x_lo;
@@ -60,7 +63,13 @@ struct TraceOperands {
     float* x_sum;     // [ceil(B / 16)][n_in]
     float* t_sum;     // [ceil(B / 16)][n_out]
     int32_t n_ks;     // k-steps per unit block: ceil(max_batch / 16)
+    int32_t paired;   // PairMode: with complement pairs, x^T over input HCUs (see above)
 };
+
+// How the trace kernels treat the input units.  kPairsSplit is kPairs for a small layer: the
+// active-block kernel then runs each contraction twice, in two waves that store the first and
+// the second rows of the pairs (see trace_active_pair_kernel).
+enum PairMode { kUnpaired = 0, kPairs = 1, kPairsSplit = 2 };
 
 // Element offset (bf16 units) of the fragment chunk that holds batch rows 8 h .. 8 h + 7 of unit
 // u in k-step ks (16 bytes, 8 consecutive rows).
@@ -83,7 +92,9 @@ constexpr int32_t kMaxActiveUnits = 12288;
 // disjoint elements of Pij:
 //   Pij <- c1 Pij + c2 sum_b x[b,i] t[b,j];  Pi, Pj from the batch means (read *_old, write
 //   *_new); w on active blocks; b = bias_gain log(max(Pj_new, eps)).  The batch enters as the
-//   split operands and column sums written by the support kernel.
+//   split operands and column sums written by the support kernel.  With complement pairs the
+//   contraction covers the first unit 2p of each input HCU, and the second takes
+//   sum_b x[b,2p+1] t[b,j] = sum_b t[b,j] - sum_b x[b,2p] t[b,j].
 struct TraceArgs {
     TraceOperands ops;
     int32_t B;
@@ -105,8 +116,8 @@ hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const Trac
                                const int32_t* act_list, const int32_t* act_count,
                                int32_t max_active, hipEvent_t start = nullptr,
                                hipEvent_t stop = nullptr);
-// Workgroups of that launch (for the launch-size check).
-int64_t trace_active_workgroups(const Geometry& g, int32_t max_active);
+// Workgroups of that launch (for the launch-size check); paired is a PairMode.
+int64_t trace_active_workgroups(const Geometry& g, int32_t max_active, int paired);
 // The elements of silent blocks over several consecutive batches: each element is read once,
 // takes the batches' updates Pij <- c1 Pij + c2 T in order (rounded to the storage format after
 // each, exactly as per-batch updates), and is written once.  Reads the mask; Pi, Pj, w and b
@@ -117,6 +128,7 @@ struct SweepBatch {
     const uint16_t* x_lo;
     const uint16_t* t_hi;
     const uint16_t* t_lo;
+    const float* t_sum;   // column sums of t per 16-row tile (read with complement pairs)
     int32_t nk;       // k-steps of this batch: ceil(B / 16)
     float c1, c2;     // 1 - a_eff and a_eff / B
 };
@@ -124,6 +136,7 @@ struct SweepArgs {
     SweepBatch bt[kMaxSweepBatches];
     int32_t n_batches;
     int32_t n_ks;     // k-steps per unit block of the operand arrays
+    int32_t paired;   // PairMode (the sweep treats kPairs and kPairsSplit alike)
     float* pij;
     const uint8_t* mask;
     int drop_bits;

@@ -225,7 +225,10 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             sum += xcol[r];
         }
         if (i < c1) {
-            write_split_column(xcol, ops.x_hi, ops.x_lo, i, rt, ops.n_ks);
+            // with complement pairs only the first unit of each input HCU enters the
+            // contraction, at the HCU's index; every unit keeps its column sum
+            if (!ops.paired) write_split_column(xcol, ops.x_hi, ops.x_lo, i, rt, ops.n_ks);
+            else if ((i & 1) == 0) write_split_column(xcol, ops.x_hi, ops.x_lo, i >> 1, rt, ops.n_ks);
             ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
         }
     };
@@ -381,7 +384,8 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     // Contraction operands of this workgroup's share of the batch (rows row0 .. row0 + 15, one
     // k-step): the hidden HCU's columns of t (the activity above, or the target) and the input
     // columns [c0, c1) of x, each column split into bf16 hi / lo parts and written in fragment
-    // order, plus the column sums over these rows.  Rows past B are written as zeros.
+    // order (of x, with complement pairs, the first unit of each input HCU), plus the column
+    // sums over these rows.  Rows past B are written as zeros.
     // The t columns go out in halves of 8 rows (one 16-byte fragment chunk of hi and of lo per
     // half), so that 2 M_out threads share the work; the two halves of a column sit in
     // neighbouring lanes and add their row sums with one lane exchange.

@@ -71,6 +71,8 @@ constexpr int kWaves = 4;           // waves (32 x 32 blocks) per workgroup, alo
 constexpr int kChunk = 4;           // k-steps (16 batch rows each) of operands per round trip
 constexpr int kActiveChunk = 8;     // the same in the active kernel (few waves: one round trip
                                     // covers a batch of 128)
+constexpr int kPairChunk = 2;       // the same in the small sweep with complement pairs (its
+                                    // registers also hold both rows of each input HCU)
 constexpr int kSums = 8;            // column-sum tiles requested up front (the batch for B <= 128)
 constexpr int kSweepRows = 16;      // row blocks per sweep over the column groups (tiled sweep)
 constexpr int64_t kStripeBytes = 3 << 19;  // t fragments an XCD keeps in L2 (persistent sweep)
@@ -118,15 +120,48 @@ __device__ __forceinline__ void marginal_request(MarginalIn& m, const float* sum
     m.p_old = p_old[u];
 }
 
-// P = c1 P_old + a_eff * (column sum / B); the same operations in the same order everywhere.
-__device__ __forceinline__ float marginal_value(const MarginalIn& m, const float* sums, int64_t st,
-                                                int u, int nk, const TraceArgs& a) {
+// Column sum over the batch: the 16-row tile sums added in tile order, starting from zero.
+// Every kernel forms a column's sum in this order, so all of them get the same bits.
+__device__ __forceinline__ float marginal_colsum(const MarginalIn& m, const float* sums,
+                                                 int64_t st, int u, int nk) {
     float colsum = 0.0f;
 #pragma unroll
     for (int q = 0; q < kSums; ++q)
         if (q < nk) colsum += m.part[q];
     for (int q = kSums; q < nk; ++q) colsum += sums[q * st + u];     // batches above 128
+    return colsum;
+}
+
+// P = c1 P_old + a_eff * (column sum / B); the same operations in the same order everywhere.
+__device__ __forceinline__ float marginal_from_colsum(const MarginalIn& m, float colsum,
+                                                      const TraceArgs& a) {
     return fmaf(a.a_eff, colsum * a.inv_b, a.c1 * m.p_old);
+}
+
+__device__ __forceinline__ float marginal_value(const MarginalIn& m, const float* sums, int64_t st,
+                                                int u, int nk, const TraceArgs& a) {
+    return marginal_from_colsum(m, marginal_colsum(m, sums, st, u, nk), a);
+}
+
+// Marginal traces and bias of unit v of the layer (rows first, then columns): the work of the
+// workgroups past the blocks in the active-block kernels.
+__device__ __forceinline__ void store_marginal(const Geometry& g, const TraceArgs& a, int64_t v,
+                                               int nk) {
+    const int n_in = (int)g.n_in, n_out = (int)g.n_out;
+    if (v >= (int64_t)n_in + n_out) return;
+    const bool is_row = v < n_in;
+    const int u = is_row ? (int)v : (int)(v - n_in);
+    const float* sums = is_row ? a.ops.x_sum : a.ops.t_sum;
+    const int64_t st = is_row ? n_in : n_out;
+    MarginalIn m;
+    marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
+    const float p = marginal_value(m, sums, st, u, nk, a);
+    if (is_row) {
+        a.pi_new[u] = p;
+    } else {
+        a.pj_new[u] = p;
+        a.b[u] = a.bias_gain * fast_log(fmaxf(p, a.eps));
+    }
 }
 
 // Silent sweep: every 32 x 32 block of Pij, updated by the contractions of a.n_batches
@@ -244,15 +279,12 @@ trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int stripe) {
 // Mask of the lane's column over a 32 x 32 block's rows, one bit per row (rows i0 .. i0 + rows - 1,
 // columns j0 .. j0 + cols - 1), as in the sweep below: one byte per lane and one ballot when the
 // block's columns fall in at most two hidden HCUs, else the bytes of the lane's 16 elements.
-__device__ __forceinline__ uint32_t block_mask_bits(const Geometry& g, const uint8_t* mask,
-                                                    int i0, int rows, int j0, int cols,
-                                                    int lane) {
+// hu: in lanes 0..31 the input HCU of block row lane, in lanes 32..63 the hidden HCU of block
+// column lane - 32 (both clamped into the layer).
+__device__ __forceinline__ uint32_t block_mask_bits_hu(const Geometry& g, const uint8_t* mask,
+                                                       int hu, int lane) {
     const int jl = lane & 31;
     const int il0 = 4 * (lane >> 5);
-    const bool is_row = lane < 32;
-    const int u = is_row ? i0 + (lane < rows ? lane : rows - 1)
-                         : j0 + (lane - 32 < cols ? lane - 32 : cols - 1);
-    const int hu = is_row ? u / g.in_mcu : u / g.out_mcu;
     const int hj = __shfl(hu, 32 + jl, 64);
     const int hc0 = __shfl(hu, 32, 64), hc1 = __shfl(hu, 63, 64);
     uint32_t bits32 = 0;
@@ -270,6 +302,15 @@ __device__ __forceinline__ uint32_t block_mask_bits(const Geometry& g, const uin
         }
     }
     return bits32;
+}
+
+__device__ __forceinline__ uint32_t block_mask_bits(const Geometry& g, const uint8_t* mask,
+                                                    int i0, int rows, int j0, int cols,
+                                                    int lane) {
+    const bool is_row = lane < 32;
+    const int u = is_row ? i0 + (lane < rows ? lane : rows - 1)
+                         : j0 + (lane - 32 < cols ? lane - 32 : cols - 1);
+    return block_mask_bits_hu(g, mask, is_row ? u / g.in_mcu : u / g.out_mcu, lane);
 }
 
 // Silent sweep of a large layer: one 128 x 128 tile (4 x 4 blocks) per workgroup of four waves,
@@ -461,21 +502,7 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
     const int nk = (a.B + 15) / 16;
     const int n_ks = a.ops.n_ks;
     if ((int)blockIdx.x >= n_work) {
-        const int64_t v = (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x;
-        if (v >= (int64_t)n_in + n_out) return;
-        const bool is_row = v < n_in;
-        const int u = is_row ? (int)v : (int)(v - n_in);
-        const float* sums = is_row ? a.ops.x_sum : a.ops.t_sum;
-        const int64_t st = is_row ? n_in : n_out;
-        MarginalIn m;
-        marginal_request(m, sums, st, u, nk, is_row ? a.pi_old : a.pj_old);
-        const float p = marginal_value(m, sums, st, u, nk, a);
-        if (is_row) {
-            a.pi_new[u] = p;
-        } else {
-            a.pj_new[u] = p;
-            a.b[u] = a.bias_gain * fast_log(fmaxf(p, a.eps));
-        }
+        store_marginal(g, a, (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x, nk);
         return;
     }
     // The x fragment pieces of the block rows (32 gathered units), the same for the four waves,
@@ -614,13 +641,506 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
     }
 }
 
+
+// ---- complement pairs ----------------------------------------------------------------------
+// Every input HCU p holds units 2p (x) and 2p + 1 (1 - x).  The kernels below contract only the
+// first units, whose split operands the support kernel wrote indexed by p, and update both rows:
+//   Pij[2p][j]     <- c1 Pij + c2 T[p][j]
+//   Pij[2p + 1][j] <- c1 Pij + c2 (S[j] - T[p][j]),   S[j] = sum_b t[b][j]
+// S is the column total in tile order (marginal_colsum).  A wave's 32 x 32 contraction over 32
+// input HCUs and 32 columns then updates 64 x 32 elements: half the matrix-core work and half
+// the x operand traffic per element.  Result register r of lane l belongs to input HCU
+// 8 (r / 4) + 4 (l / 32) + r % 4 of the block, as in the kernels above.
+
+// Silent sweep with complement pairs (small layers): trace_sweep_kernel over blocks of 32 input
+// HCUs (64 rows).
+template <int kDropBits>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(3, 3)))
+trace_sweep_pair_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int stripe) {
+    const int lane = threadIdx.x & 63;
+    const int n_out = (int)g.n_out;
+    const int n_pb = (g.in_hcu + 31) / 32;
+    for (int item = blockIdx.x; item < n_work; item += gridDim.x) {
+        // the order of trace_sweep_kernel, over blocks of input HCUs
+        const int wg = (int)xcd_linear_index(item, n_work);
+        const int s0 = wg / (n_pb * stripe) * stripe;
+        const int in_stripe = wg - s0 * n_pb;
+        const int groups_here = n_cg - s0 < stripe ? n_cg - s0 : stripe;
+        const int bi = in_stripe / groups_here;
+        const int bj = (s0 + in_stripe % groups_here) * kWaves + (threadIdx.x >> 6);
+        const int p0 = bi * 32, j0 = bj * 32;
+        if (j0 >= n_out) continue;                                 // wave-uniform; no barriers
+        const int prs = g.in_hcu - p0 < 32 ? g.in_hcu - p0 : 32;   // input HCUs of the block
+        const int cols = n_out - j0 < 32 ? n_out - j0 : 32;
+        const int n_ks = a.n_ks;
+        const int jl = lane & 31;
+        const int il0 = 4 * (lane >> 5);
+        const int jc = j0 + (jl < cols ? jl : cols - 1);           // the lane's column (clamped)
+
+        // rows 2 p0 .. 2 (p0 + prs) - 1; a row past them is out of the buffer range
+        const rsrc_t rp = make_rsrc(a.pij + (int64_t)(2 * p0) * n_out,
+                                    (uint32_t)(2 * prs) * n_out * 4u);
+        const uint32_t o0 = ((uint32_t)(2 * il0) * n_out + j0 + jl) * 4u;
+        const uint32_t odd = (uint32_t)n_out * 4u;
+        float pe[16], po[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t off = o0 + (uint32_t)(2 * (8 * (r >> 2) + (r & 3))) * n_out * 4u;
+            pe[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off, 0, 0));
+            po[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off + odd, 0, 0));
+        }
+        const int hu = lane < 32 ? p0 + (lane < prs ? lane : prs - 1) : jc / g.out_mcu;
+        const uint32_t act_bits = block_mask_bits_hu(g, a.mask, hu, lane);
+
+        const int64_t fa = ((int64_t)bi * n_ks * 64 + lane) * 8;
+        const int64_t fb = ((int64_t)bj * n_ks * 64 + lane) * 8;
+        for (int t = 0; t < a.n_batches; ++t) {
+            const SweepBatch bt = a.bt[t];
+            const int nk = bt.nk;
+            // the column total's first tile sums, requested ahead of the contraction
+            MarginalIn m;
+#pragma unroll
+            for (int q = 0; q < kSums; ++q)
+                m.part[q] = bt.t_sum[(int64_t)(q < nk ? q : nk - 1) * n_out + jc];
+            f16v acc = {};
+            for (int k0 = 0; k0 < nk; k0 += kPairChunk) {
+                u32x4 op[kPairChunk][4];
+#pragma unroll
+                for (int c = 0; c < kPairChunk; ++c) {
+                    const int64_t ks = (int64_t)(k0 + c < nk ? k0 + c : nk - 1) * 512;
+                    op[c][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa + ks);
+                    op[c][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa + ks);
+                    op[c][2] = *reinterpret_cast<const u32x4*>(bt.t_hi + fb + ks);
+                    op[c][3] = *reinterpret_cast<const u32x4*>(bt.t_lo + fb + ks);
+                }
+#pragma unroll
+                for (int c = 0; c < kPairChunk; ++c) {
+                    if (k0 + c < nk) {
+                        const bf8 ah = __builtin_bit_cast(bf8, op[c][0]);
+                        const bf8 al = __builtin_bit_cast(bf8, op[c][1]);
+                        const bf8 bh = __builtin_bit_cast(bf8, op[c][2]);
+                        const bf8 bl = __builtin_bit_cast(bf8, op[c][3]);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc, 0, 0, 0);
+                        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc, 0, 0, 0);
+                    }
+                }
+            }
+            const float st = marginal_colsum(m, bt.t_sum, n_out, jc, nk);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                pe[r] = to_storage<kDropBits>(fmaf(bt.c2, acc[r], bt.c1 * pe[r]));
+                po[r] = to_storage<kDropBits>(fmaf(bt.c2, st - acc[r], bt.c1 * po[r]));
+            }
+        }
+
+        // ---- epilogue: the elements of silent blocks, unconditional buffer stores -------------
+        const bool jok = jl < cols;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const uint32_t off = o0 + (uint32_t)(2 * (8 * (r >> 2) + (r & 3))) * n_out * 4u;
+            const bool keep = jok && !((act_bits >> il) & 1u);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pe[r]), rp,
+                                                  keep ? off : kDrop, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(po[r]), rp,
+                                                  keep ? off + odd : kDrop, 0, 0);
+        }
+    }
+}
+
+// Silent sweep with complement pairs (large layers): trace_sweep_tile_kernel with wave w on
+// block w of 32 input HCUs (64 rows) and two column blocks, a workgroup on 128 input HCUs x 64
+// columns.  The column totals of every queued batch are formed once per workgroup into LDS.
+template <int kDropBits, int kKC>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
+    constexpr int kCB = 2;                          // column blocks per workgroup
+    constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
+    constexpr int kPerWave = kItems / kWaves;
+    static_assert(kPerWave * kWaves == kItems, "t items split evenly over the waves");
+    __shared__ u32x4 stage[2][kItems][64];
+    __shared__ float stot[kMaxSweepBatches][32 * kCB];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n_out = (int)g.n_out;
+    const int n_pb = (g.in_hcu + 31) / 32, n_cb = (n_out + 31) / 32;
+    const int n_ti = (n_pb + 3) / 4;
+    constexpr int kSweepTiles = kSweepRows / 4;
+    const int wg = (int)xcd_linear_index(blockIdx.x, gridDim.x);
+    const int sweep = wg / (kSweepTiles * n_tj);
+    const int in_sweep = wg % (kSweepTiles * n_tj);
+    const int here = n_ti - sweep * kSweepTiles < kSweepTiles ? n_ti - sweep * kSweepTiles
+                                                              : kSweepTiles;
+    const int ti = sweep * kSweepTiles + in_sweep % here;
+    const int tj = in_sweep / here;
+    const int n_ks = a.n_ks;
+
+    const int bi = 4 * ti + wave;
+    const int bic = bi < n_pb ? bi : n_pb - 1;
+    const int p0 = bic * 32;
+    const int prs = g.in_hcu - p0 < 32 ? g.in_hcu - p0 : 32;
+    const bool live = bi < n_pb;                           // wave-uniform
+    const int j00 = kCB * tj * 32;
+    const int jl = lane & 31, il0 = 4 * (lane >> 5);
+    const rsrc_t rp = make_rsrc(a.pij + (int64_t)(2 * p0) * n_out, (uint32_t)(2 * prs) * n_out * 4u);
+    const uint32_t o0 = ((uint32_t)(2 * il0) * n_out + j00 + jl) * 4u;
+    const uint32_t odd = (uint32_t)n_out * 4u;
+    float pold[kCB][2][16];
+#pragma unroll
+    for (int c = 0; c < kCB; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t off =
+                o0 + (uint32_t)(2 * (8 * (r >> 2) + (r & 3)) * n_out + 32 * c) * 4u;
+            pold[c][0][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off, 0, 0));
+            pold[c][1][r] =
+                __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off + odd, 0, 0));
+        }
+    uint32_t act_bits[kCB];
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) {
+        const int j0 = j00 + 32 * c;
+        const int jc = j0 < n_out ? j0 : (n_cb - 1) * 32;
+        const int cols = n_out - jc < 32 ? n_out - jc : 32;
+        const int hu = lane < 32 ? p0 + (lane < prs ? lane : prs - 1)
+                                 : (jc + (lane - 32 < cols ? lane - 32 : cols - 1)) / g.out_mcu;
+        act_bits[c] = block_mask_bits_hu(g, a.mask, hu, lane);
+    }
+
+    int n_ch = 0;
+    for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
+    // requests of the chunk at (batch t, first k-step k0): the t items into stage buffer sb
+    // (item = (k-step in chunk * kCB + column block) * 2 + {hi, lo}, wave w issuing w, w + 4,
+    // ...) and this wave's x fragments into xn
+    u32x4 xc[kKC][2], xn[kKC][2];
+    auto request = [&](int t, int k0, int sb) {
+        const SweepBatch bt = a.bt[t];
+#pragma unroll
+        for (int q = 0; q < kPerWave; ++q) {
+            const int item = wave + kWaves * q;
+            const int half = item & 1, cb = (item >> 1) % kCB, kq = item / (2 * kCB);
+            int blk = kCB * tj + cb;
+            blk = blk < n_cb ? blk : n_cb - 1;
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
+                                  (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
+            __builtin_amdgcn_global_load_lds((const void*)src,
+                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+        }
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const int64_t fa = (((int64_t)bic * n_ks + ks) * 64 + lane) * 8;
+            xn[kq][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa);
+            xn[kq][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa);
+        }
+    };
+    auto next = [&](int& t, int& k0) {
+        k0 += kKC;
+        if (k0 >= a.bt[t].nk) { k0 = 0; ++t; }
+    };
+
+    int dt = 0, dk = 0;
+    request(dt, dk, 0);
+    next(dt, dk);
+
+    // column totals of every queued batch for the workgroup's 32 kCB columns (clamped)
+    for (int e = threadIdx.x; e < a.n_batches * 32 * kCB; e += kWaves * 64) {
+        const int t = e / (32 * kCB), cl = e % (32 * kCB);
+        const int col = j00 + cl < n_out ? j00 + cl : n_out - 1;
+        const SweepBatch bt = a.bt[t];
+        MarginalIn m;
+#pragma unroll
+        for (int q = 0; q < kSums; ++q)
+            m.part[q] = bt.t_sum[(int64_t)(q < bt.nk ? q : bt.nk - 1) * n_out + col];
+        stot[t][cl] = marginal_colsum(m, bt.t_sum, n_out, col, bt.nk);
+    }
+    lds_barrier();
+
+    f16v acc[kCB];
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) acc[c] = f16v{};
+    int ct = 0, ck = 0;
+    for (int lc = 0; lc < n_ch; ++lc) {
+        // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
+        // items visible to every wave and tells that every wave is done with the other buffer
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            xc[kq][0] = xn[kq][0];
+            xc[kq][1] = xn[kq][1];
+        }
+        stage_barrier();
+        if (lc + 1 < n_ch) {
+            request(dt, dk, (lc + 1) & 1);
+            next(dt, dk);
+        }
+        const int sb = lc & 1;
+        const int nk = a.bt[ct].nk;
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            if (ck + kq < nk) {
+                const bf8 ah = __builtin_bit_cast(bf8, xc[kq][0]);
+                const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
+                bf8 bh[kCB], bl[kCB];
+#pragma unroll
+                for (int c = 0; c < kCB; ++c) {
+                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2][lane]);
+                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
+                }
+#pragma unroll
+                for (int c = 0; c < kCB; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[c], acc[c], 0, 0, 0);
+#pragma unroll
+                for (int c = 0; c < kCB; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl[c], acc[c], 0, 0, 0);
+#pragma unroll
+                for (int c = 0; c < kCB; ++c)
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[c], acc[c], 0, 0, 0);
+            }
+        }
+        if (ck + kKC >= nk) {
+            const float c1 = a.bt[ct].c1, c2 = a.bt[ct].c2;
+#pragma unroll
+            for (int c = 0; c < kCB; ++c) {
+                const float st = stot[ct][32 * c + jl];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    pold[c][0][r] = to_storage<kDropBits>(fmaf(c2, acc[c][r], c1 * pold[c][0][r]));
+                    pold[c][1][r] =
+                        to_storage<kDropBits>(fmaf(c2, st - acc[c][r], c1 * pold[c][1][r]));
+                }
+                acc[c] = f16v{};
+            }
+        }
+        next(ct, ck);
+    }
+    if (!live) return;
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) {
+        const bool jok = j00 + 32 * c + jl < n_out;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const uint32_t off =
+                o0 + (uint32_t)(2 * (8 * (r >> 2) + (r & 3)) * n_out + 32 * c) * 4u;
+            const bool keep = jok && !((act_bits[c] >> il) & 1u);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pold[c][0][r]), rp,
+                                                  keep ? off : kDrop, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pold[c][1][r]), rp,
+                                                  keep ? off + odd : kDrop, 0, 0);
+        }
+    }
+}
+
+// Active blocks with complement pairs: trace_active_kernel with the block rows taken as 32 of
+// the hidden HCU's active input HCUs (64 rows), their first units gathered through the active
+// list.  kSplit (small layers, where the kernel is bound by latency rather than by its matrix
+// work): a workgroup covers two column blocks, and each block's contraction is run by two
+// waves, one storing the first rows of the pairs and one the second, so that every wave keeps
+// the per-element work of the unpaired kernel.  Otherwise a workgroup covers four column blocks
+// and each wave stores both rows.
+template <int kDropBits, bool kSplit>
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+trace_active_pair_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_list,
+                         const int32_t* __restrict__ act_count, int n_rt, int n_cgr,
+                         int n_work) {
+    __builtin_amdgcn_s_setprio(3);
+    const int n_in = (int)g.n_in, n_out = (int)g.n_out;
+    const int nk = (a.B + 15) / 16;
+    const int n_ks = a.ops.n_ks;
+    if ((int)blockIdx.x >= n_work) {
+        store_marginal(g, a, (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x, nk);
+        return;
+    }
+    constexpr int kBlocks = kSplit ? kWaves / 2 : kWaves;     // column blocks per workgroup
+    __shared__ u32x4 xs[kActiveChunk][2][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int par = kSplit ? (wave & 1) : 0;                  // the rows a split wave stores
+    const int wg = (int)xcd_linear_index(blockIdx.x, n_work);
+    const int per_hcu = n_rt * n_cgr;
+    const int hj = wg / per_hcu;
+    const int rt = (wg - hj * per_hcu) / n_cgr;
+    const int c0 = ((wg - hj * per_hcu - rt * n_cgr) * kBlocks + (kSplit ? wave >> 1 : wave)) * 32;
+    const bool col_live = c0 < g.out_mcu;                      // wave-uniform
+    const int cols = col_live ? (g.out_mcu - c0 < 32 ? g.out_mcu - c0 : 32) : 1;
+    const int j0 = hj * g.out_mcu + (col_live ? c0 : 0);
+    const int jl = lane & 31;
+    const int il0 = 4 * (lane >> 5);
+    const int h = lane >> 5;
+    const int jb = j0 + (jl < cols ? jl : cols - 1);
+
+    // the active count (in input HCUs) and the list entry of block row jl, then the columns
+    const int k_total = act_count[hj];
+    const int kr = rt * 32 + jl < g.in_hcu ? rt * 32 + jl : g.in_hcu - 1;
+    const int hsel = act_list[(int64_t)hj * g.in_hcu + kr];
+    u32x4 opt[kActiveChunk][2], opx[kActiveChunk][2];
+    auto load_t = [&](int k0) {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            const int64_t fb = frag_chunk(jb, k0 + c < nk ? k0 + c : nk - 1, h, n_ks);
+            opt[c][0] = *reinterpret_cast<const u32x4*>(a.ops.t_hi + fb);
+            opt[c][1] = *reinterpret_cast<const u32x4*>(a.ops.t_lo + fb);
+        }
+    };
+    constexpr int kGather = kActiveChunk * 2 * 64 / (kWaves * 64);
+    auto gather_x = [&](int k0, int pa) {
+        u32x4 v[kGather];
+#pragma unroll
+        for (int q = 0; q < kGather; ++q) {
+            const int P = threadIdx.x + kWaves * 64 * q;
+            const int hp = (P >> 5) & 1, hl = (P >> 6) & 1, kq = P >> 7;
+            const int ks = k0 + kq < nk ? k0 + kq : nk - 1;
+            const int64_t fa = frag_chunk(pa, ks, hp, n_ks);
+            v[q] = *reinterpret_cast<const u32x4*>((hl ? a.ops.x_lo : a.ops.x_hi) + fa);
+        }
+#pragma unroll
+        for (int q = 0; q < kGather; ++q) {
+            const int P = threadIdx.x + kWaves * 64 * q;
+            xs[P >> 7][(P >> 6) & 1][P & 63] = v[q];
+        }
+    };
+    auto load_x = [&]() {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            opx[c][0] = xs[c][0][lane];
+            opx[c][1] = xs[c][1][lane];
+        }
+    };
+    f16v acc = {};
+    auto contract = [&](int k0) {
+#pragma unroll
+        for (int c = 0; c < kActiveChunk; ++c) {
+            if (k0 + c < nk) {
+                const bf8 ah = __builtin_bit_cast(bf8, opx[c][0]);
+                const bf8 al = __builtin_bit_cast(bf8, opx[c][1]);
+                const bf8 bh = __builtin_bit_cast(bf8, opt[c][0]);
+                const bf8 bl = __builtin_bit_cast(bf8, opt[c][1]);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc, 0, 0, 0);
+            }
+        }
+    };
+    load_t(0);
+
+    // input HCU of block row jl (the A-operand row of this lane), clamped into the layer
+    const int pa = hsel < 0 ? 0 : (hsel < g.in_hcu ? hsel : g.in_hcu - 1);
+    int pr[16];
+    float pe[16], po[kSplit ? 1 : 16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        pr[r] = half_broadcast(pa, 8 * (r >> 2) + (r & 3), lane);
+        if constexpr (kSplit) {
+            pe[r] = a.pij[(int64_t)(2 * pr[r] + par) * n_out + jb];
+        } else {
+            pe[r] = a.pij[(int64_t)(2 * pr[r]) * n_out + jb];
+            po[r] = a.pij[(int64_t)(2 * pr[r] + 1) * n_out + jb];
+        }
+    }
+    gather_x(0, pa);
+    // marginal inputs.  Split: lanes 0..31 the stored unit of row jl's input HCU, 32..63 the
+    // block's columns.  Otherwise: lane l the unit 2 pa + l / 32 (both units of row jl's input
+    // HCU), and every lane its own column.
+    const bool row_lane = kSplit ? lane < 32 : true;
+    const int urow = kSplit ? 2 * pa + par : 2 * pa + (lane >> 5);
+    MarginalIn mr, mc;
+    if constexpr (kSplit) {
+        marginal_request(mr, row_lane ? a.ops.x_sum : a.ops.t_sum, row_lane ? n_in : n_out,
+                         row_lane ? urow : jb, nk, row_lane ? a.pi_old : a.pj_old);
+    } else {
+        marginal_request(mr, a.ops.x_sum, n_in, urow, nk, a.pi_old);
+        marginal_request(mc, a.ops.t_sum, n_out, jb, nk, a.pj_old);
+    }
+
+    lds_barrier();
+    load_x();
+    contract(0);
+    for (int k0 = kActiveChunk; k0 < nk; k0 += kActiveChunk) {   // batches above 128 rows
+        lds_barrier();
+        load_t(k0);
+        gather_x(k0, pa);
+        lds_barrier();
+        load_x();
+        contract(k0);
+    }
+    if (!col_live) return;
+    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
+    const bool jok = jl < cols;
+
+    if constexpr (kSplit) {
+        const float* sums = row_lane ? a.ops.x_sum : a.ops.t_sum;
+        const int64_t st_m = row_lane ? n_in : n_out;
+        const int um = row_lane ? urow : jb;
+        const float cs = marginal_colsum(mr, sums, st_m, um, nk);
+        const float lp = fast_log(fmaxf(marginal_from_colsum(mr, cs, a), a.eps));
+        const float lpj = __shfl(lp, 32 + jl, 64);
+        const float st = __shfl(cs, 32 + jl, 64);          // column total of t
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int src = 8 * (r >> 2) + (r & 3);
+            const int il = il0 + src;
+            const float lpi = half_broadcast(lp, src, lane);
+            const float tv = par ? st - acc[r] : acc[r];
+            const float pn = to_storage<kDropBits>(fmaf(a.c2, tv, a.c1 * pe[r]));
+            const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
+            if (jok && il < rows) {
+                const int64_t e = (int64_t)(2 * pr[r] + par) * n_out + jb;
+                a.pij[e] = pn;
+                a.w[e] = wv;
+            }
+        }
+    } else {
+        const float lp = fast_log(fmaxf(marginal_value(mr, a.ops.x_sum, n_in, urow, nk, a), a.eps));
+        const float st = marginal_colsum(mc, a.ops.t_sum, n_out, jb, nk);
+        const float lpj = fast_log(fmaxf(marginal_from_colsum(mc, st, a), a.eps));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int src = 8 * (r >> 2) + (r & 3);
+            const int il = il0 + src;
+            const float lpe = half_broadcast(lp, src, lane);        // first unit of HCU il
+            const float lpo = half_broadcast(lp, 32 + src, lane);   // second unit
+            const float ne = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pe[r]));
+            const float no = to_storage<kDropBits>(fmaf(a.c2, st - acc[r], a.c1 * po[r]));
+            const float we = to_storage<kDropBits>(fast_log(fmaxf(ne, a.eps)) - lpe - lpj);
+            const float wo = to_storage<kDropBits>(fast_log(fmaxf(no, a.eps)) - lpo - lpj);
+            if (jok && il < rows) {
+                const int64_t e = (int64_t)(2 * pr[r]) * n_out + jb;
+                a.pij[e] = ne;
+                a.w[e] = we;
+                a.pij[e + n_out] = no;
+                a.w[e + n_out] = wo;
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const SweepArgs& a,
                               int64_t resident_wgs, hipEvent_t start, hipEvent_t stop) {
     if (a.n_batches < 1 || a.n_batches > kMaxSweepBatches) return hipErrorInvalidValue;
-    const int64_t n_rb = (g.n_in + 31) / 32, n_cb = (g.n_out + 31) / 32;
+    if (a.paired && g.in_mcu != 2) return hipErrorInvalidValue;
+    // row blocks: 32 input units, or with complement pairs 32 input HCUs (64 rows)
+    const int64_t n_rb = a.paired ? (g.in_hcu + 31) / 32 : (g.n_in + 31) / 32;
+    const int64_t n_cb = (g.n_out + 31) / 32;
     const int64_t n_cg = (n_cb + kWaves - 1) / kWaves;
+    if (resident_wgs < 0 && a.paired) {
+        // large layer: 128 input HCUs x 64 columns per workgroup
+        void (*kernel)(Geometry, SweepArgs, int) = nullptr;
+        switch (a.drop_bits) {
+            case 0: kernel = trace_sweep_pair_tile_kernel<0, kTileKC>; break;
+            case 13: kernel = trace_sweep_pair_tile_kernel<13, kTileKC>; break;
+            case 16: kernel = trace_sweep_pair_tile_kernel<16, kTileKC>; break;
+            default: return hipErrorInvalidValue;
+        }
+        const int64_t n_ti = (n_rb + 3) / 4, n_tj = (n_cb + 1) / 2;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(kWaves * 64), 0, stream,
+                              start, stop, 0, g, a, (int)n_tj);
+        return hipGetLastError();
+    }
     if (resident_wgs < 0) {
         // large layer: 128 x 128 tiles, operands staged through LDS
         void (*kernel)(Geometry, SweepArgs, int) = nullptr;
@@ -636,10 +1156,13 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
         return hipGetLastError();
     }
     void (*kernel)(Geometry, SweepArgs, int, int, int) = nullptr;
-    switch (a.drop_bits) {
+    switch (a.drop_bits * 2 + (a.paired ? 1 : 0)) {
         case 0: kernel = trace_sweep_kernel<0>; break;
-        case 13: kernel = trace_sweep_kernel<13>; break;
-        case 16: kernel = trace_sweep_kernel<16>; break;
+        case 26: kernel = trace_sweep_kernel<13>; break;
+        case 32: kernel = trace_sweep_kernel<16>; break;
+        case 1: kernel = trace_sweep_pair_kernel<0>; break;
+        case 27: kernel = trace_sweep_pair_kernel<13>; break;
+        case 33: kernel = trace_sweep_pair_kernel<16>; break;
         default: return hipErrorInvalidValue;
     }
     const int64_t n_work = n_rb * n_cg;
@@ -659,24 +1182,42 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
     return hipGetLastError();
 }
 
-int64_t trace_active_workgroups(const Geometry& g, int32_t max_active) {
-    const int64_t n_rt = ((int64_t)max_active * g.in_mcu + 31) / 32;
-    const int64_t n_cgr = ((g.out_mcu + 31) / 32 + kWaves - 1) / kWaves;
+// Row tiles of a hidden HCU's active rows (32 units, or with complement pairs 32 input HCUs)
+// and column groups of a hidden HCU (four 32-column blocks, two when pair rows are split).
+static int64_t active_row_tiles(const Geometry& g, int32_t max_active, int paired) {
+    return paired ? ((int64_t)max_active + 31) / 32 : ((int64_t)max_active * g.in_mcu + 31) / 32;
+}
+static int64_t active_col_groups(const Geometry& g, int paired) {
+    const int per = paired == kPairsSplit ? kWaves / 2 : kWaves;
+    return ((g.out_mcu + 31) / 32 + per - 1) / per;
+}
+
+int64_t trace_active_workgroups(const Geometry& g, int32_t max_active, int paired) {
+    const int64_t n_rt = active_row_tiles(g, max_active, paired);
+    const int64_t n_cgr = active_col_groups(g, paired);
     return (int64_t)g.out_hcu * n_rt * n_cgr + (g.n_in + g.n_out + kWaves * 64 - 1) / (kWaves * 64);
 }
 
 hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const TraceArgs& a,
                                const int32_t* act_list, const int32_t* act_count,
                                int32_t max_active, hipEvent_t start, hipEvent_t stop) {
-    const int64_t n_rt = ((int64_t)max_active * g.in_mcu + 31) / 32;
-    const int64_t n_cgr = ((g.out_mcu + 31) / 32 + kWaves - 1) / kWaves;
+    const int paired = a.ops.paired;
+    if (paired && g.in_mcu != 2) return hipErrorInvalidValue;
+    const int64_t n_rt = active_row_tiles(g, max_active, paired);
+    const int64_t n_cgr = active_col_groups(g, paired);
     const int64_t n_work = (int64_t)g.out_hcu * n_rt * n_cgr;
-    const int64_t blocks = trace_active_workgroups(g, max_active);
+    const int64_t blocks = trace_active_workgroups(g, max_active, paired);
     void (*kernel)(Geometry, TraceArgs, const int32_t*, const int32_t*, int, int, int) = nullptr;
-    switch (a.drop_bits) {
+    switch (a.drop_bits * 4 + paired) {
         case 0: kernel = trace_active_kernel<0>; break;
-        case 13: kernel = trace_active_kernel<13>; break;
-        case 16: kernel = trace_active_kernel<16>; break;
+        case 52: kernel = trace_active_kernel<13>; break;
+        case 64: kernel = trace_active_kernel<16>; break;
+        case 1: kernel = trace_active_pair_kernel<0, false>; break;
+        case 53: kernel = trace_active_pair_kernel<13, false>; break;
+        case 65: kernel = trace_active_pair_kernel<16, false>; break;
+        case 2: kernel = trace_active_pair_kernel<0, true>; break;
+        case 54: kernel = trace_active_pair_kernel<13, true>; break;
+        case 66: kernel = trace_active_pair_kernel<16, true>; break;
         default: return hipErrorInvalidValue;
     }
     hipExtLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kWaves * 64), 0, stream, start,

@@ -72,6 +72,9 @@ class Workload:
     readout_mcu: int = 0      # classes of a supervised readout layer (0 = none)
     readout_epochs: int = 0
     storage: str = "f32"      # storage format of Pij and W: "f32", "bf16", "m10"
+    # the inputs are pixels encoded as complementary pairs (x, 1 - x) (encode_pixels), which a
+    # layer may exploit in its joint-trace contraction (bcpnn_config.complement_pairs)
+    complement_pairs: bool = True
 
 
 def _mnist_like(name: str, **kw) -> Workload:

@@ -42,8 +42,8 @@ def oracle_params(cfg) -> oracle.Params:
 def workload_config(w: synth.Workload, max_batch=None, **kw):
     L = w.layer
     base = dict(alpha=w.alpha, gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
-                seed=w.seed_noise,
-                storage=w.storage)
+                seed=w.seed_noise, storage=w.storage,
+                complement_pairs=int(w.complement_pairs))
     base.update(kw)
     return gpu_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, max_batch or w.batch, **base)
 

@@ -41,6 +41,7 @@ def test_default_config(b):
     assert (c.in_hcu, c.in_mcu, c.out_hcu, c.out_mcu, c.max_batch) == (784, 2, 30, 100, 128)
     assert c.alpha == pytest.approx(1e-3) and c.n_cycles == 1 and c.gain == 1.0
     assert c.eps == pytest.approx(1e-8) and c.n_swaps == 1 and c.storage == 0
+    assert c.complement_pairs == 0
 
 
 BAD = {
@@ -64,6 +65,8 @@ BAD = {
     "storage unknown": dict(storage=7),
     "pi_init above 1": dict(pi_init=2.0),
     "noise negative": dict(init_noise=-0.1),
+    "complement pairs of 3 MCUs": dict(in_mcu=3, complement_pairs=1),
+    "complement pairs flag 2": dict(complement_pairs=2),
 }
 
 

@@ -82,6 +82,14 @@ CASES = {
     "mnist_b96_tail": (MNIST, {}, 96, False),
     "mnist_bf16": (MNIST, dict(storage="bf16"), 128, False),
     "mnist_m10": (MNIST, dict(storage="m10"), 128, False),
+    # the same without exploiting the (x, 1 - x) input pairs: every input unit contracted
+    "tiny_unpaired": (TINY, dict(complement_pairs=0), 32, False),
+    "tiny_unpaired_ragged_13": (TINY, dict(complement_pairs=0), 13, False),
+    "tiny_unpaired_supervised": (TINY, dict(complement_pairs=0), 32, True),
+    "mnist_unpaired_b128": (MNIST, dict(complement_pairs=0), 128, False),
+    "mnist_unpaired_b96_tail": (MNIST, dict(complement_pairs=0), 96, False),
+    "mnist_unpaired_bf16": (MNIST, dict(storage="bf16", complement_pairs=0), 128, False),
+    "mnist_unpaired_m10": (MNIST, dict(storage="m10", complement_pairs=0), 128, False),
 }
 
 
@@ -317,17 +325,27 @@ SHAPES = {
     "single_hidden_mcu": (25, 2, 40, 1, 5, 20),
     "batch_200": (40, 2, 4, 24, 20, 200),          # 13 row tiles: past the 8 summed up front
     "batch_256_odd_mcus": (33, 3, 5, 7, 11, 256),  # M_out 7 (scalar weight rows), 16 k-steps
+    # (x, 1 - x) input pairs exploited by the trace kernels (complement_pairs = 1)
+    "pairs_wide_200": (30, 2, 3, 200, 12, 33),
+    "pairs_batch_200": (40, 2, 4, 24, 20, 200),
+    "pairs_single_hidden_mcu": (25, 2, 40, 1, 5, 20),
+    "pairs_many_active": (70, 2, 3, 40, 61, 48),   # two 32-HCU row tiles per hidden HCU
 }
 
 
 @pytest.mark.parametrize("shape", list(SHAPES))
 def test_other_shapes_one_step(shape):
     hin, min_, hout, mout, k, B = SHAPES[shape]
+    pairs = shape.startswith("pairs_")
     rng = np.random.default_rng(sum(map(ord, shape)))
     mask = np.stack([synth.random_mask(hin, 1, k, 50 + c)[:, 0] for c in range(hout)], 1)
-    pair = Pair(gpu_config(hin, min_, hout, mout, B, alpha=0.05, gain=2.0), mask)
-    a = rng.random((20 * B, hin, min_)) + 0.05
-    X = (a / a.sum(-1, keepdims=True)).reshape(20 * B, -1).astype(np.float32)
+    pair = Pair(gpu_config(hin, min_, hout, mout, B, alpha=0.05, gain=2.0,
+                           complement_pairs=int(pairs)), mask)
+    if pairs:
+        X = synth.encode_pixels(rng.random((20 * B, hin)).astype(np.float32))
+    else:
+        a = rng.random((20 * B, hin, min_)) + 0.05
+        X = (a / a.sum(-1, keepdims=True)).reshape(20 * B, -1).astype(np.float32)
     pretrain(pair, X, 15, B, alpha=0.1)
     y, s, y_o, s_o = pair.forward(X[:B])
     assert_support_close(s, s_o)
@@ -342,10 +360,11 @@ def test_other_shapes_one_step(shape):
     pair.close()
 
 
-def test_stl_shape_sampled():
+@pytest.mark.parametrize("pairs", [1, 0])
+def test_stl_shape_sampled(pairs):
     """The STL-shaped layer at full size (55296 x 10000 traces, 5% receptive fields, batch 256)
-    in the launch configuration the benchmark uses: one structural update, one batch and the
-    whole-matrix weight pass, checked on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
+    in the launch configuration the benchmark uses (complement pairs; also without): one
+    structural update, one batch and the whole-matrix weight pass, checked on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
     from the GPU's prior weights, and the sampled blocks of the traces and weights from the
     prior state restricted to the sampled input and hidden HCUs (the trace and weight updates
     are elementwise given the batch, so a sub-problem reproduces them exactly)."""
@@ -354,7 +373,7 @@ def test_stl_shape_sampled():
     px, _ = synth.dataset(w, n=256)
     x = synth.encode_pixels(px)
     mask = workload_mask(w)
-    cfg = workload_config(w)
+    cfg = workload_config(w, complement_pairs=pairs)
     from pairs import bcpnn
     t = __import__("torch")
     layer = bcpnn().Layer(cfg, mask)

@@ -39,14 +39,16 @@ def _inputs():
     return out
 
 
-def test_sweep_grouping_is_bitwise_invisible():
+@pytest.mark.parametrize("pairs", [1, 0])
+def test_sweep_grouping_is_bitwise_invisible(pairs):
     """The same batches, with a structural update before the twelfth, run freely and with the
     state read after every batch: bitwise identical states."""
     import torch
     xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()]
     states = []
     for read_each in (False, True):
-        layer = bcpnn().Layer(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
+        layer = bcpnn().Layer(workload_config(MNIST, alpha=0.02, complement_pairs=pairs),
+                              workload_mask(MNIST))
         for k, x in enumerate(xs):
             if k == STRUCTURAL_AT:
                 layer.structural_update(count=False)
@@ -59,12 +61,13 @@ def test_sweep_grouping_is_bitwise_invisible():
         assert np.array_equal(states[0][key].view(np.uint8), states[1][key].view(np.uint8)), key
 
 
-def test_multi_batch_run_matches_oracle():
+@pytest.mark.parametrize("pairs", [1, 0])
+def test_multi_batch_run_matches_oracle(pairs):
     """Target-clamped batches (the traces then depend on the inputs alone, with no feedback
     through the weights), no re-synchronisation: after 20 batches the state agrees with the
     oracle to the per-step tolerances; a forward pass mid-run does not disturb the sweeps."""
     rng = np.random.default_rng(5)
-    pair = Pair(workload_config(MNIST, alpha=0.02), workload_mask(MNIST))
+    pair = Pair(workload_config(MNIST, alpha=0.02, complement_pairs=pairs), workload_mask(MNIST))
     cfg = pair.cfg
     t = pair.torch
     for k, x in enumerate(_inputs()):
@@ -126,15 +129,17 @@ def test_state_calls_between_batches_see_every_update():
     torch.cuda.synchronize()
 
 
-def test_tiled_sweep_on_a_ragged_large_layer():
-    """A layer just past the size at which the library sweeps silent blocks in 128 x 128
-    workgroup tiles (257 x 66 blocks of 32: ragged row and column tiles), ten target-clamped
-    batches of mixed size (one sweep of eight, two pending), against the oracle."""
+@pytest.mark.parametrize("pairs", [1, 0])
+def test_tiled_sweep_on_a_ragged_large_layer(pairs):
+    """A layer just past the size at which the library sweeps silent blocks in workgroup tiles
+    (257 x 66 blocks of 32: ragged row and column tiles), ten target-clamped batches of mixed
+    size (one sweep of eight, two pending), against the oracle."""
     from pairs import gpu_config
     in_hcu, out_hcu, out_mcu = 4100, 21, 100
     rng = np.random.default_rng(11)
     mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0] for c in range(out_hcu)], 1)
-    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05), mask)
+    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05, complement_pairs=pairs),
+                mask)
     for B in (64, 64, 40, 64, 23, 64, 1, 64, 64, 50):
         p = rng.random((B, in_hcu)).astype(np.float32)
         x = synth.encode_pixels(p)
