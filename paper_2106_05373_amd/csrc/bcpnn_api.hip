@@ -224,11 +224,16 @@ hipError_t launch_pending_sweep(bcpnn_layer* L) {
     if (e != hipSuccess) return e;
     const int64_t seq = L->n_sweeps++;
     const int slot = (int)(seq % kSets);
-    e = hipEventRecord(L->sweep_ready, L->stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->sweep_ready, 0);
-    if (e == hipSuccess)
-        e = bcpnn::launch_trace_sweep(L->side, L->g, a, L->sweep_wgs, t0, t1);
-    if (e == hipSuccess) e = hipEventRecord(L->sweep_done[slot], L->side);
+    // A small layer's sweep overlaps the next batches on the side stream.  A large layer's
+    // tiled sweep runs in order on the caller's stream: it fills the machine, and beside it
+    // the support and active-block kernels lose more time than the overlap gains.
+    hipStream_t s = L->sweep_wgs < 0 ? L->stream : L->side;
+    if (s != L->stream) {
+        e = hipEventRecord(L->sweep_ready, L->stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, L->sweep_ready, 0);
+    }
+    if (e == hipSuccess) e = bcpnn::launch_trace_sweep(s, L->g, a, L->sweep_wgs, t0, t1);
+    if (e == hipSuccess) e = hipEventRecord(L->sweep_done[slot], s);
     if (e != hipSuccess) return e;
     for (int t = 0; t < L->n_pend; ++t) L->set_sweep[L->pend[t].set] = seq;
     L->n_pend = 0;

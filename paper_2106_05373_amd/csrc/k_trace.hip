@@ -336,6 +336,7 @@ __device__ __forceinline__ void stage_barrier() {
 constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 constexpr int kTileKC = 2;
+constexpr int kPairTileCB = 3;   // column blocks per workgroup of the tiled sweep with pairs
 
 template <int kDropBits, int kKC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -752,10 +753,9 @@ trace_sweep_pair_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int strip
 // Silent sweep with complement pairs (large layers): trace_sweep_tile_kernel with wave w on
 // block w of 32 input HCUs (64 rows) and two column blocks, a workgroup on 128 input HCUs x 64
 // columns.  The column totals of every queued batch are formed once per workgroup into LDS.
-template <int kDropBits, int kKC>
+template <int kDropBits, int kKC, int kCB>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
-    constexpr int kCB = 2;                          // column blocks per workgroup
     constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kWaves;
     static_assert(kPerWave * kWaves == kItems, "t items split evenly over the waves");
@@ -883,18 +883,19 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
             if (ck + kq < nk) {
                 const bf8 ah = __builtin_bit_cast(bf8, xc[kq][0]);
                 const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
-                bf8 bh[kCB], bl[kCB];
+                // the hi parts of t stay for two passes, each lo part is read for its one
+                bf8 bh[kCB];
 #pragma unroll
-                for (int c = 0; c < kCB; ++c) {
+                for (int c = 0; c < kCB; ++c)
                     bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2][lane]);
-                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
-                }
 #pragma unroll
                 for (int c = 0; c < kCB; ++c)
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[c], acc[c], 0, 0, 0);
 #pragma unroll
-                for (int c = 0; c < kCB; ++c)
-                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl[c], acc[c], 0, 0, 0);
+                for (int c = 0; c < kCB; ++c) {
+                    const bf8 bl = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[c], 0, 0, 0);
+                }
 #pragma unroll
                 for (int c = 0; c < kCB; ++c)
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh[c], acc[c], 0, 0, 0);
@@ -1131,12 +1132,13 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
         // large layer: 128 input HCUs x 64 columns per workgroup
         void (*kernel)(Geometry, SweepArgs, int) = nullptr;
         switch (a.drop_bits) {
-            case 0: kernel = trace_sweep_pair_tile_kernel<0, kTileKC>; break;
-            case 13: kernel = trace_sweep_pair_tile_kernel<13, kTileKC>; break;
-            case 16: kernel = trace_sweep_pair_tile_kernel<16, kTileKC>; break;
+            case 0: kernel = trace_sweep_pair_tile_kernel<0, kTileKC, kPairTileCB>; break;
+            case 13: kernel = trace_sweep_pair_tile_kernel<13, kTileKC, kPairTileCB>; break;
+            case 16: kernel = trace_sweep_pair_tile_kernel<16, kTileKC, kPairTileCB>; break;
             default: return hipErrorInvalidValue;
         }
-        const int64_t n_ti = (n_rb + 3) / 4, n_tj = (n_cb + 1) / 2;
+        const int64_t n_ti = (n_rb + 3) / 4;
+        const int64_t n_tj = (n_cb + kPairTileCB - 1) / kPairTileCB;
         hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(kWaves * 64), 0, stream,
                               start, stop, 0, g, a, (int)n_tj);
         return hipGetLastError();
