@@ -203,9 +203,13 @@ hipError_t timer_events(bcpnn_layer* L, int k, hipEvent_t* start, hipEvent_t* st
     return hipSuccess;
 }
 
-// Enqueues the silent-element sweep of the pending batches on the side stream, after the
-// caller's stream has written their operands.
-hipError_t launch_pending_sweep(bcpnn_layer* L) {
+hipError_t wait_sweep(bcpnn_layer* L, int64_t seq);
+
+// Enqueues the silent-element sweep of the pending batches, after the caller's stream has
+// written their operands.  join: the caller's stream is about to wait for it (a state access or
+// a structural update), so the sweep runs there, after every earlier sweep, over the whole
+// machine.
+hipError_t launch_pending_sweep(bcpnn_layer* L, bool join = false) {
     if (L->n_pend == 0) return hipSuccess;
     bcpnn::SweepArgs a{};
     for (int t = 0; t < L->n_pend; ++t) {
@@ -222,17 +226,20 @@ hipError_t launch_pending_sweep(bcpnn_layer* L) {
     hipEvent_t t0 = nullptr, t1 = nullptr;
     hipError_t e = timer_events(L, BCPNN_KERNEL_SWEEP, &t0, &t1);
     if (e != hipSuccess) return e;
+    // A small layer's sweep overlaps the next batches on the side stream, one workgroup per CU.
+    // A large layer's tiled sweep runs in order on the caller's stream: it fills the machine,
+    // and beside it the support and active-block kernels lose more time than the overlap gains.
+    const bool in_order = join || L->sweep_wgs < 0;
+    hipStream_t s = in_order ? L->stream : L->side;
+    const int64_t wgs = in_order && L->sweep_wgs > 0 ? 0 : L->sweep_wgs;
+    if (in_order && L->n_sweeps > 0) e = wait_sweep(L, L->n_sweeps - 1);   // earlier sweeps
     const int64_t seq = L->n_sweeps++;
     const int slot = (int)(seq % kSets);
-    // A small layer's sweep overlaps the next batches on the side stream.  A large layer's
-    // tiled sweep runs in order on the caller's stream: it fills the machine, and beside it
-    // the support and active-block kernels lose more time than the overlap gains.
-    hipStream_t s = L->sweep_wgs < 0 ? L->stream : L->side;
-    if (s != L->stream) {
+    if (e == hipSuccess && s != L->stream) {
         e = hipEventRecord(L->sweep_ready, L->stream);
         if (e == hipSuccess) e = hipStreamWaitEvent(s, L->sweep_ready, 0);
     }
-    if (e == hipSuccess) e = bcpnn::launch_trace_sweep(s, L->g, a, L->sweep_wgs, t0, t1);
+    if (e == hipSuccess) e = bcpnn::launch_trace_sweep(s, L->g, a, wgs, t0, t1);
     if (e == hipSuccess) e = hipEventRecord(L->sweep_done[slot], s);
     if (e != hipSuccess) return e;
     for (int t = 0; t < L->n_pend; ++t) L->set_sweep[L->pend[t].set] = seq;
@@ -251,7 +258,7 @@ hipError_t wait_sweep(bcpnn_layer* L, int64_t seq) {
 // Applies the pending silent updates and makes the caller's stream wait for the last sweep:
 // every Pij is then current in stream order.
 hipError_t join_side(bcpnn_layer* L) {
-    hipError_t e = launch_pending_sweep(L);
+    hipError_t e = launch_pending_sweep(L, true);
     if (e == hipSuccess && L->n_sweeps > 0) e = wait_sweep(L, L->n_sweeps - 1);
     return e;
 }
