@@ -20,34 +20,60 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kMaxSwaps = 256;
 
-// One wave per block.  Lane l sums columns l, l + 64, ... of the block (each over the block's
-// rows in order), then a butterfly adds the 64 partial sums.  Waves of a workgroup take
-// neighbouring hidden HCUs of the same input HCU, i.e. neighbouring column spans of the same
-// Pij rows.
+// kGroup lanes per block, 64 / kGroup blocks per wave (consecutive blocks: neighbouring hidden
+// HCUs of one input HCU, i.e. neighbouring column spans of the same Pij rows).  Lane k of a
+// group sums the block's columns k, k + kGroup, ..., kColChunk columns at a time (their loads
+// issued together), each chunk row by row; an xor butterfly over the group then adds the
+// partial sums, leaving the same bits in every lane of the group.  The pattern depends only on
+// positions inside the block.  Few lanes per block keep the lanes busy with fp64 log terms
+// (M_out = 100: 13 columns per lane for 8 lanes) rather than with per-block reductions.
+constexpr int kGroup = 8;
+constexpr int kColChunk = 4;
+
 __global__ void __launch_bounds__(kThreads)
 mi_kernel(Geometry g, const float* __restrict__ pi, const float* __restrict__ pj,
           const float* __restrict__ pij, float eps, double* __restrict__ mi) {
     const int lane = threadIdx.x & 63;
-    const int64_t blk = (int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-    if (blk >= (int64_t)g.in_hcu * g.out_hcu) return;          // whole wave
-    const int64_t hi = blk / g.out_hcu;
-    const int64_t hj = blk % g.out_hcu;
+    const int sub = lane % kGroup;
+    const int64_t n_blk = (int64_t)g.in_hcu * g.out_hcu;
+    const int64_t blk = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) *
+                            (64 / kGroup) + lane / kGroup;
+    if (((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * (64 / kGroup) >= n_blk)
+        return;                                                   // whole wave
+    const bool live = blk < n_blk;
+    const int64_t b = live ? blk : n_blk - 1;                     // clamped lanes still reduce
+    const int64_t hi = b / g.out_hcu;
+    const int64_t hj = b - hi * g.out_hcu;
     const double e = (double)eps;
     double part = 0.0;
-    for (int c = lane; c < g.out_mcu; c += 64) {
-        const int64_t j = hj * g.out_mcu + c;
-        const double pjc = fmax((double)pj[j], e);
+    for (int c0 = sub; c0 < g.out_mcu; c0 += kGroup * kColChunk) {
+        double pjc[kColChunk];
+#pragma unroll
+        for (int k = 0; k < kColChunk; ++k) {
+            const int c = c0 + k * kGroup;
+            pjc[k] = c < g.out_mcu ? fmax((double)pj[hj * g.out_mcu + c], e) : 1.0;
+        }
         for (int m = 0; m < g.in_mcu; ++m) {
             const int64_t i = hi * g.in_mcu + m;
-            const float q = pij[i * g.n_out + j];
-            if (q != 0.0f) {
-                const double den = fmax((double)pi[i], e) * pjc;
-                part += (double)q * log(fmax((double)q, e) / den);
+            const double pim = fmax((double)pi[i], e);
+            float q[kColChunk];
+#pragma unroll
+            for (int k = 0; k < kColChunk; ++k) {
+                const int c = c0 + k * kGroup;
+                q[k] = c < g.out_mcu ? pij[i * g.n_out + hj * g.out_mcu + c] : 0.0f;
+            }
+#pragma unroll
+            for (int k = 0; k < kColChunk; ++k) {
+                if (q[k] != 0.0f) {
+                    const double den = pim * pjc[k];
+                    part += (double)q[k] * log(fmax((double)q[k], e) / den);
+                }
             }
         }
     }
-    part = wave_sum(part);
-    if (lane == 0) mi[blk] = part;
+#pragma unroll
+    for (int off = kGroup / 2; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
+    if (live && sub == 0) mi[blk] = part;
 }
 
 struct Pick {
@@ -181,7 +207,8 @@ swap_kernel(Geometry g, const double* __restrict__ mi, int32_t n_swaps,
 
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
                                      const float* pj, const float* pij, float eps, double* mi) {
-    const int64_t blocks = ((int64_t)g.in_hcu * g.out_hcu + 3) / 4;
+    const int64_t per_wg = (int64_t)(kThreads / 64) * (64 / kGroup);
+    const int64_t blocks = ((int64_t)g.in_hcu * g.out_hcu + per_wg - 1) / per_wg;
     mi_kernel<<<(unsigned)blocks, kThreads, 0, stream>>>(g, pi, pj, pij, eps, mi);
     return hipGetLastError();
 }
