@@ -48,12 +48,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 22008730,
-    ("stl", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 2406025873,
+    ("mnist", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 21995002,
+    ("stl", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 2405963998,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 121059635,
-    ("stl", "a02df3cea6181c1c62bec0f33eaa7b56eaafe4663f6e88f1e6284533258fb289"): 19677732193,
+    ("mnist", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 92423643,
+    ("stl", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 10060685372,
 }
 
 
