@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 METRIC = "train samples/s, MNIST-shaped 30x100 BCPNN layer; % MFMA peak, HBM GB/s"
 PEAK_HBM_GBS = 8000.0
 PEAK_F64_MFMA_TFS = 78.6
+PEAK_F32_MFMA_TFS = 157.3
 # Every PROFILE_PERIOD-th launch of each train_batch kernel in the timed steps carries
 # dispatch-stamped events; a timed launch costs its stream a few microseconds, so sampling keeps
 # the throughput honest.
@@ -300,6 +301,25 @@ def main():
         "timed_launches": wp_n,
     }
 
+    # ---- the two products at their dense size, against the fp32 matrix-core peak -------------
+    # What a dense fp32 implementation would run per batch: the support X (W o mask) and the
+    # contraction X^T Y over every element, 2 B N_in N_out flops each.  Here the support skips
+    # silent blocks (fp64) and the contraction runs as split bf16 (over half the rows with
+    # complement pairs), so these rates are dense-equivalent: the dense product's flops over
+    # the time the kernels take to deliver its result (support: its event-timed duration;
+    # contraction: the sweep's time per batch plus the active-block kernel's).
+    dense_flops = 2.0 * avg_b * L.n_in * L.n_out
+    act_s = act_ms / 1e3 / max(act_n, 1)
+    trace_s = avg_sweep_s / per_sweep + act_s
+    dense_equivalent = {
+        "unit": "TFLOP/s", "peak": PEAK_F32_MFMA_TFS, "flops_per_batch": dense_flops,
+        "support": round(dense_flops / avg_sup_s / 1e12, 2) if sup_n else None,
+        "support_frac": round(dense_flops / avg_sup_s / 1e12 / PEAK_F32_MFMA_TFS, 3)
+                        if sup_n else None,
+        "trace": round(dense_flops / trace_s / 1e12, 2),
+        "trace_frac": round(dense_flops / trace_s / 1e12 / PEAK_F32_MFMA_TFS, 3),
+    }
+
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
@@ -320,6 +340,7 @@ def main():
         "mfma": mfma,
         "critical_path": critical_path,
         "weight_pass": weight_pass,
+        "dense_equivalent": dense_equivalent,
     }
 
     if not args.no_cpu_baseline and args.cpu_seconds > 0:
