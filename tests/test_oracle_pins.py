@@ -232,6 +232,24 @@ def test_trace_invariants_hold_at_every_step():
                                    np.repeat(L.pj[None, :], 64, 0), atol=2e-7)
 
 
+def test_complementary_pair_rows_sum_to_the_column_mean():
+    # Inputs encoded as (x, 1 - x) pairs: the batch means of the two rows of a pair add up to
+    # the hidden unit's batch mean, <x a_j> + <(1 - x) a_j> = <a_j> -- the identity by which the
+    # GPU path derives the second row of each pair from the column total.  With rate 1 the
+    # traces are the batch means themselves.  x on a 1/256 grid makes 1 - x exact in fp32.
+    rng = np.random.default_rng(12)
+    p = P(in_hcu=5, in_mcu=2, out_hcu=3, out_mcu=4, alpha=1.0)
+    L = trained_layer(p, steps=2)
+    xe = rng.integers(0, 257, size=(9, 5)).astype(np.float32) / 256
+    x = synth.encode_pixels(xe)
+    assert np.array_equal(x[:, 0::2] + x[:, 1::2], np.ones_like(xe))
+    y = rng.random((9, 12)).astype(np.float32)
+    _, pj, pij = oracle.update_traces(p, x, y, L.pi, L.pj, L.pij)
+    pair_sum = pij[0::2].astype(np.float64) + pij[1::2].astype(np.float64)
+    np.testing.assert_allclose(pair_sum, np.broadcast_to(pj, pair_sum.shape), rtol=2e-7)
+    np.testing.assert_allclose(pj, y.astype(np.float64).mean(0), rtol=1e-7)
+
+
 # ------------------------------------------------------------------------------------------
 # Weights, bias and mask
 # ------------------------------------------------------------------------------------------
