@@ -17,8 +17,12 @@
 //        HCU's active input units, gathered) together with their weights, and the marginal
 //        traces and bias of every unit: everything the next batch's support reads;
 //      - the silent kernel sweeps the whole matrix and stores the elements of silent blocks.
-//    The library runs the silent kernel on a second stream, where it overlaps the next batch's
-//    support kernel (which never reads silent elements); every state access waits for it.
+//    For a small layer the library runs the silent kernel on a second stream, where it overlaps
+//    the next batch's support kernel (which never reads silent elements); every state access
+//    waits for it.  A large layer's sweep runs in order on the caller's stream.
+//  * With complement pairs (every input HCU holds x and 1 - x) the contraction covers the first
+//    unit of each pair and the second row takes the column total minus it (the *_pair_*
+//    kernels below), halving the matrix work and the x operand traffic.
 //  * T runs on the bf16 matrix cores with a two-term split of both operands: v = hi + lo with
 //    hi = bf16(v), lo = bf16(v - hi), and T ~ lo.hi' + hi.lo' + hi.hi' (three
 //    v_mfma_f32_32x32x16_bf16, fp32 accumulation).  Each product is then exact to about 3
