@@ -49,12 +49,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 21995002,
-    ("stl", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 2405963998,
+    ("mnist", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 22005207,
+    ("stl", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 2406046576,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 92423643,
-    ("stl", "15f6cbf85c8297c846f4bbe46a39a6db14cd44ac6669cc9dbe9be6147cdbf965"): 10060685372,
+    ("mnist", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 92394414,
+    ("stl", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 10069177642,
 }
 
 
