@@ -755,8 +755,9 @@ trace_sweep_pair_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int strip
 }
 
 // Silent sweep with complement pairs (large layers): trace_sweep_tile_kernel with wave w on
-// block w of 32 input HCUs (64 rows) and two column blocks, a workgroup on 128 input HCUs x 64
-// columns.  The column totals of every queued batch are formed once per workgroup into LDS.
+// block w of 32 input HCUs (64 rows) and kCB column blocks, a workgroup on 128 input HCUs x
+// 32 kCB columns (the library uses three: 96 columns).  The column totals of every queued
+// batch are formed once per workgroup into LDS.
 template <int kDropBits, int kKC, int kCB>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
