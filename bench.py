@@ -49,12 +49,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 22005207,
-    ("stl", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 2406046576,
+    ("mnist", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 21996977,
+    ("stl", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 2406033541,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 92394414,
-    ("stl", "8c34d57d6eea4ab460aaf0704ccc581604821bebd33751a8b9637a8051406408"): 10069177642,
+    ("mnist", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 92771215,
+    ("stl", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 10081990651,
 }
 
 
