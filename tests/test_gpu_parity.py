@@ -330,6 +330,7 @@ SHAPES = {
     "pairs_batch_200": (40, 2, 4, 24, 20, 200),
     "pairs_single_hidden_mcu": (25, 2, 40, 1, 5, 20),
     "pairs_many_active": (70, 2, 3, 40, 61, 48),   # two 32-HCU row tiles per hidden HCU
+    "pairs_batch_512": (24, 2, 3, 16, 9, 512),     # 32 k-steps: four active-kernel chunks
 }
 
 
