@@ -49,12 +49,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 21996977,
-    ("stl", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 2406033541,
+    ("mnist", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 22006951,
+    ("stl", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 2406000508,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 92771215,
-    ("stl", "461c60f7902dc241583c13eb6e5c146667fe0bc6fe314c3d464eb51a1b49c878"): 10081990651,
+    ("mnist", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 92600723,
+    ("stl", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 10127353714,
 }
 
 
