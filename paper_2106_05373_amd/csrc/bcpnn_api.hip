@@ -56,7 +56,6 @@ struct bcpnn_layer {
     int32_t* act_count = nullptr;        // [out_hcu]
     int32_t* swap_count = nullptr;       // [out_hcu]
     double* mi = nullptr;                // [in_hcu][out_hcu]
-    float* y_buf = nullptr;              // [max_batch][n_out] activity when the caller gives none
     // Split batch operands of the joint-trace contraction, kSets sets used in turn.  The silent
     // elements of Pij take the updates of up to kMaxSweepBatches consecutive batches in one
     // sweep on the side stream, which reads those batches' sets while later batches proceed.
@@ -161,7 +160,7 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
 void free_layer(bcpnn_layer* L) {
     if (!L) return;
     void* bufs[] = {L->pi[0], L->pi[1], L->pj[0], L->pj[1], L->pij, L->w, L->b, L->mask,
-                    L->act_list, L->act_count, L->swap_count, L->mi, L->y_buf};
+                    L->act_list, L->act_count, L->swap_count, L->mi};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int k = 0; k < kSets; ++k) {
@@ -352,7 +351,6 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = dalloc(&L->act_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->swap_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->mi, hh);
-    if (e == hipSuccess) e = dalloc(&L->y_buf, (size_t)cfg->max_batch * g.n_out);
     // split operands in fragment order: 1 KiB per 32 units and 16 batch rows; the units past
     // the layer in the last block are never written and must read as zero
     const int32_t n_ks = (cfg->max_batch + 15) / 16;
@@ -462,7 +460,7 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     if (misaligned(x_dev) || misaligned(target_dev) || misaligned(y_dev))
         return fail(BCPNN_EINVAL, "device buffers must be 16-byte aligned");
     if (bcpnn_status st = check_batch(L, B)) return st;
-    float* y = y_dev ? y_dev : L->y_buf;
+    float* y = y_dev;                    // nullable: the activities then stay on the chip
     const int set = L->ops_cur;
     // the operand set is free once the sweep that read it last has run
     if (L->set_sweep[set] >= 0) HIP_TRY(L, wait_sweep(L, L->set_sweep[set]));

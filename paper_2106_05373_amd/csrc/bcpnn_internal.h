@@ -43,7 +43,7 @@ hipError_t launch_apply_mask(hipStream_t stream, const Geometry& g, const uint8_
                              float* w);
 
 // Support over the active input HCUs (fp64 MFMA) followed by, per (sample, hidden HCU):
-//   mode 0: softmax with gain -> y (and s if non-null);
+//   mode 0: softmax with gain -> y if non-null (and s if non-null);
 //   mode 1: argmax -> winner (and s if non-null).
 // max_active is the largest number of active input HCUs of any hidden HCU (swaps keep it).
 // With ops non-null (training), the kernel also writes the contraction operands: the split

@@ -354,8 +354,8 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
                     const float ya = ea[q] * ia, yb = eb[q] * ib;
                     sa[m] = ya;                       // kept for the contraction operands
                     sb[m] = yb;
-                    if (va) y[oa + m] = ya;
-                    if (vb) y[ob + m] = yb;
+                    if (y && va) y[oa + m] = ya;   // training may not ask for them
+                    if (y && vb) y[ob + m] = yb;
                 }
             }
         } else {
