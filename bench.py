@@ -49,12 +49,12 @@ WEIGHT_PASSES = 20
 # workload and the SHA-256 of the library sources it was measured on (source_digest).  A
 # changed source reports null until measured again.
 MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 22006951,
-    ("stl", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 2406000508,
+    ("mnist", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 21994518,
+    ("stl", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 2406070970,
 }
 MEASURED_TRAFFIC = {
-    ("mnist", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 92600723,
-    ("stl", "c4b42bee392ed3b6a10a36fd415e0bbb59c87dca274f0a759a8daca4ec779e80"): 10127353714,
+    ("mnist", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 92670958,
+    ("stl", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 10024194360,
 }
 
 
@@ -248,8 +248,8 @@ def main():
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
         "kernel": "silent-block trace sweep (the x^T t contractions of up to "
                   f"{SWEEP_BATCHES} consecutive batches on split-bf16 MFMA, one read and one write "
-                  "of Pij; on a second stream overlapping later batches: one workgroup per CU "
-                  "for a small layer, LDS-staged tiles for a large one; "
+                  "of Pij; a small layer: one workgroup per CU on a second stream overlapping "
+                  "later batches; a large layer: LDS-staged tiles on the caller's stream; "
                   + ("trace_sweep_pair_kernel / trace_sweep_pair_tile_kernel: over the first "
                      "unit of each (x, 1 - x) input pair, the second row from the column total)"
                      if pairs else "trace_sweep_kernel / trace_sweep_tile_kernel)"),
