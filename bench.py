@@ -93,9 +93,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2345, help="timed batches (5 epochs = 2345)")
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="mnist", choices=["mnist", "stl", "mnist_pipeline"],
-                    help="mnist / stl: hidden-layer training (the metric); mnist_pipeline: the "
-                         "hidden layer plus a supervised readout, then held-out inference")
+    ap.add_argument("--workload", default="mnist",
+                    choices=["mnist", "stl", "stl_shard8", "mnist_pipeline"],
+                    help="mnist / stl: hidden-layer training (the metric); stl_shard8: one GPU's "
+                         "share of the STL-shaped layer sharded by hidden HCU over eight GPUs; "
+                         "mnist_pipeline: the hidden layer plus a supervised readout, then "
+                         "held-out inference")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU-oracle baseline sample (0 = skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -101,6 +101,11 @@ WORKLOADS = {
     "stl": Workload(name="stl", data="textures96", n_train=5000,
                     layer=LayerShape(27648, 2, 100, 100), batch=256, alpha=1e-3, epochs=1,
                     mask_frac=0.05, period=20),
+    # One GPU's share of the STL-shaped layer sharded by hidden HCU over eight GPUs: 13 of the
+    # 100 hidden HCUs against the whole input (the per-shard kernels at their real shape).
+    "stl_shard8": Workload(name="stl_shard8", data="textures96", n_train=5000,
+                           layer=LayerShape(27648, 2, 13, 100), batch=256, alpha=1e-3, epochs=1,
+                           mask_frac=0.05, period=20),
     # MNIST-shaped layer with Pij and W stored in bf16, or with a 10-bit mantissa.
     "mnist_bf16": _mnist_like("mnist_bf16", storage="bf16"),
     "mnist_m10": _mnist_like("mnist_m10", storage="m10"),
