@@ -8,14 +8,20 @@ fields, batch 128, alpha 1e-3, structural plasticity before every 100th batch of
 A step is one batch of that schedule: the structural update when it is due (MI score + greedy
 swap), then support, per-HCU softmax, trace, weight and bias updates.  The whole dataset, one
 shuffled copy per epoch touched, is staged in HBM before timing.  W warm-up steps run first;
-then exactly K steps are timed between two device synchronisations.
+then exactly K steps are timed between two device synchronisations.  The timed region ends
+with bcpnn_flush, so the silent-block trace updates of every timed batch (which the library
+queues and applies a few batches at a time) are inside it, and no kernel in it carries
+profiling events.
 
-Printed: one JSON line with the throughput (training samples/s), the roofline position of
-the dominant kernel (the sweep over the silent elements of Pij, timed over the timed steps with
-HIP events that its own dispatches stamp on the layer's side stream, on every 32nd launch), the
-fp64 matrix-core fraction of the support GEMM and the per-batch time of the caller's stream
-(support and active-block kernels, timed the same way), and the CPU oracle's throughput on a
-bounded sample of the same schedule on this host.
+After the timed region, an untimed profiling pass continues the same schedule with every
+kernel launch stamped by HIP events (dispatch-stamped, so each brackets one kernel on its own
+stream); the kernel durations of the JSON line come from it: the roofline position of the
+dominant kernel (the sweep over the silent elements of Pij), the support and active-block
+kernels of the caller's stream, and the structural update.  The line also carries the
+whole-matrix weight pass, the STL-shaped layer (a short run of the same schedule on the first
+images of that workload, with its weight pass), the forward-pass throughput by batch size, and
+the CPU oracle on a bounded sample of the MNIST-shaped schedule on this host's cores (all
+threads, and one).
 """
 from __future__ import annotations
 
@@ -34,46 +40,45 @@ sys.path.insert(0, ROOT)
 METRIC = "train samples/s, MNIST-shaped 30x100 BCPNN layer; % MFMA peak, HBM GB/s"
 PEAK_HBM_GBS = 8000.0
 PEAK_F64_MFMA_TFS = 78.6
-PEAK_F32_MFMA_TFS = 157.3
-# Every PROFILE_PERIOD-th launch of each train_batch kernel in the timed steps carries
-# dispatch-stamped events; a timed launch costs its stream a few microseconds, so sampling keeps
-# the throughput honest.
-PROFILE_PERIOD = 32
+PEAK_BF16_MFMA_TFS = 2500.0
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
 # Launches of the whole-matrix weight pass timed after the training run.
 WEIGHT_PASSES = 20
+# Structural updates timed after the profiling pass.
+STRUCTURAL_TIMED = 3
+# Forward-pass batch sizes of the inference sweep.
+INFERENCE_BATCHES = [1, 8, 32, 128, 512, 2048, 8192]
+# STL-shaped leg of the default line: warm-up and timed batches (the first images of the set).
+STL_WARMUP, STL_STEPS = 2, 16
 
 # HBM traffic per launch (bytes) of the sweep kernel and of the weight pass, from rocprofv3
 # FETCH_SIZE and WRITE_SIZE runs scaled by the copy-kernel calibration factors, keyed by
-# workload and the SHA-256 of the library sources it was measured on (source_digest).  A
-# changed source reports null until measured again.
-MEASURED_WEIGHT_TRAFFIC = {
-    ("mnist", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 21994518,
-    ("stl", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 2406070970,
-}
-MEASURED_TRAFFIC = {
-    ("mnist", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 92670958,
-    ("stl", "be04a6b27819204b1a9746f5b11f0c16cfd3847d65b3582a879336abbd5290a7"): 10024194360,
-}
+# workload and the SHA-256 of the sources of that kernel (kernel_digest).  A changed source
+# reports null until measured again.
+MEASURED_WEIGHT_TRAFFIC = {}
+MEASURED_TRAFFIC = {}
 
 
-def source_digest(csrc):
-    """SHA-256 over the library's sources (every .hip and .h file in name order): a measured
-    traffic figure holds only for the sources it was taken with."""
+def kernel_digest(csrc, files):
+    """SHA-256 over the named source files of one kernel (its .hip file and the headers it
+    includes): a measured traffic figure holds only for the sources it was taken with."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(f.read())
+    for name in files:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
+
+
+SWEEP_SOURCES = ("k_trace.hip", "bcpnn_internal.h", "device_common.h")
+WEIGHT_SOURCES = ("k_weights.hip", "bcpnn_internal.h", "device_common.h")
 
 
 def sweep_sizes(sched, first, last):
     """Batches per sweep launch over steps [first, last), mirroring the library: the pending
     batches are swept once SWEEP_BATCHES have accumulated and before every structural update;
-    the sweeps start from an empty queue (a profile read flushes it) and the rest is flushed at
-    the end."""
+    the sweeps start from an empty queue (the previous pass ended with a flush) and the rest is
+    flushed at the end."""
     sizes, pend = [], 0
     for s in range(first, last):
         if sched[s][4] and pend:
@@ -100,16 +105,24 @@ def parse():
                          "mnist_pipeline: the hidden layer plus a supervised readout, then "
                          "held-out inference")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
-                    help="time budget of the CPU-oracle baseline sample (0 = skip)")
+                    help="time budget of the all-threads CPU-oracle sample (0 = skip); the "
+                         "one-thread sample gets half of it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--launch", choices=["eager", "graph"], default="eager",
+                    help="how the steps of the timed region are issued: eager, one library call "
+                         "per step; graph, the steps' calls captured once into a HIP graph before "
+                         "the timed region and replayed once inside it.  The other way is timed "
+                         "on the following steps and reported beside it")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the MNIST-shaped line: no STL-shaped leg, no inference sweep")
     ap.add_argument("--no-pairs", action="store_true",
                     help="contract every input unit instead of exploiting the (x, 1 - x) pixel "
                          "pairs (complement_pairs = 0)")
     ap.add_argument("--precision-report", action="store_true",
-                    help="reduced-precision storage: readout-pipeline accuracy with Pij and W in "
-                         "fp32 / bf16 / 10-bit mantissa, hidden code against the fp32 oracle")
+                    help="reduced-precision storage (bf16, 10-bit mantissa) on the MNIST-shaped "
+                         "layer against the fp32 oracle: trace and weight errors, masks, codes")
     ap.add_argument("--inference-sweep", action="store_true",
-                    help="forward-pass throughput of the MNIST-shaped layer over batch sizes")
+                    help="only the forward-pass throughput of the MNIST-shaped layer by batch size")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 256 MiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -135,7 +148,6 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2106_05373_amd import bcpnn, synth
 
     if args.calibrate_copy:
         # A plain copy of known size: 256 MiB read + 256 MiB written per launch.
@@ -153,34 +165,77 @@ def main():
     if args.precision_report:
         return run_precision_report(args)
     if args.inference_sweep:
-        return run_inference_sweep(args)
+        print(json.dumps(run_inference_sweep()), flush=True)
+        return
 
+    from paper_2106_05373_amd import synth
     w = synth.WORKLOADS[args.workload]
+    pairs = 0 if args.no_pairs else int(w.complement_pairs)
+    res = measure_training(w, args.warmup, args.steps, pairs, profile_steps=None,
+                           launch=args.launch)
+
+    out = {
+        "metric": METRIC, "value": res["value"], "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic", "config": res["config"], "roofline": res["roofline"],
+        "mfma": res["mfma"], "contraction": res["contraction"],
+        "critical_path": res["critical_path"], "structural_update": res["structural_update"],
+        "weight_pass": res["weight_pass"],
+    }
+    if not args.no_extras and args.workload == "mnist":
+        stl = synth.WORKLOADS["stl"]
+        r = measure_training(stl, STL_WARMUP, STL_STEPS, int(stl.complement_pairs),
+                             profile_steps=STL_STEPS, launch=args.launch)
+        out["stl"] = {"value": r["value"], "unit": "samples/s", "ms_per_step": r["ms_per_step"],
+                      "steps": STL_STEPS, "warmup": STL_WARMUP, "config": r["config"],
+                      "roofline": r["roofline"], "critical_path": r["critical_path"],
+                      "structural_update": r["structural_update"],
+                      "weight_pass": r["weight_pass"]}
+        out["inference_sweep"] = run_inference_sweep()["sweep"]
+    if not args.no_cpu_baseline and args.cpu_seconds > 0 and args.workload == "mnist":
+        out["cpu_baseline"] = cpu_baseline(w, res["mask"], args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
+                     launch="eager"):
+    """Trains the workload's layer on its schedule: `warmup` untimed steps, `steps` timed
+    between two synchronisations (ending with bcpnn_flush), then an untimed profiling pass of
+    the following steps with every kernel dispatch-stamped, structural updates and weight
+    passes timed the same way.  Returns the fields of the JSON line."""
+    import torch
+    from paper_2106_05373_amd import bcpnn, synth
+
     L = w.layer
     B = w.batch
-    pairs = 0 if args.no_pairs else int(w.complement_pairs)
-    n_steps = args.warmup + args.steps
-    sched = schedule(w.n_train, B, w.period, n_steps)
+    if profile_steps is None:
+        profile_steps = min(max(steps, 64), 512)
+    n_train = n_images if n_images is not None else w.n_train
+    n_other = steps                  # the other launch mode, timed on the following steps
+    n_steps = warmup + steps + n_other + profile_steps
+    sched = schedule(n_train, B, w.period, n_steps)
     epochs = sorted({s[0] for s in sched})
 
     # ---- data staged on the device (not timed) -----------------------------------------
     t0 = time.time()
-    px, _ = synth.dataset(w)
+    px, _ = synth.dataset(w, n=n_images)
     X = torch.from_numpy(synth.encode_pixels(px))
     del px
     dev = torch.device("cuda", 0)
     shuffled = {}
     for e in epochs:
-        perm = torch.from_numpy(synth.epoch_permutation(w.n_train, w.seed_shuffle, e))
+        perm = torch.from_numpy(synth.epoch_permutation(n_train, w.seed_shuffle, e))
         shuffled[e] = X[perm].to(dev).contiguous()
+    del X
     k_act = synth.active_count(L.in_hcu, w.mask_frac)
     mask = synth.random_mask(L.in_hcu, L.out_hcu, k_act, w.seed_mask)
     prep_s = time.time() - t0
 
     stream = torch.cuda.Stream(device=dev)
     cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
-                               gain=w.gain, init_noise=w.init_noise, seed=w.seed_noise,
-                               complement_pairs=pairs)
+                               gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
+                               seed=w.seed_noise, complement_pairs=pairs)
     layer = bcpnn.Layer(cfg, mask, stream=stream)
 
     def step(s):
@@ -190,82 +245,125 @@ def main():
         layer.train_batch(shuffled[e][start:start + size])
 
     torch.cuda.synchronize()
-    for s in range(args.warmup):
+    for s in range(warmup):
         step(s)
+    layer.flush()
     torch.cuda.synchronize()
 
-    layer.profile_read()                          # applies pending sweeps; discards old timings
-    # every PROFILE_PERIOD-th sweep of a long run, every sweep of a short one
-    layer.profile_enable(PROFILE_PERIOD if args.steps >= 32 * PROFILE_PERIOD else 1)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    ev0.record(stream)
-    for s in range(args.warmup, n_steps):
+    # ---- the timed region: exactly `steps` steps, no profiling events ----------------------
+    def timed(a, b, how):
+        """Steps [a, b) then the flush, between two synchronisations; seconds."""
+        graph = None
+        if how == "graph":
+            # the same library calls, recorded once (nothing runs during capture)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=stream):
+                for s in range(a, b):
+                    step(s)
+                layer.flush()
+            torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        if graph is not None:
+            with torch.cuda.stream(stream):
+                graph.replay()
+        else:
+            for s in range(a, b):
+                step(s)
+            layer.flush()          # the queued silent-block updates of the timed batches
+        torch.cuda.synchronize()
+        return time.perf_counter() - t_start
+
+    first, last = warmup, warmup + steps
+    wall_s = timed(first, last, launch)
+    samples = sum(sched[s][3] for s in range(first, last))
+    plastic_steps = sum(sched[s][4] for s in range(first, last))
+    other = "graph" if launch == "eager" else "eager"
+    el = timed(last, last + n_other, other)
+    other_fig = {"launch": other,
+                 "value": round(sum(sched[s][3] for s in range(last, last + n_other)) / el, 1),
+                 "ms_per_step": round(el * 1e3 / n_other, 5),
+                 "steps": f"the {n_other} steps after the timed ones, timed the same way"}
+    last += n_other
+
+    # ---- untimed profiling pass: the following steps, every launch dispatch-stamped --------
+    for k in bcpnn.KERNELS:
+        layer.profile_read_kernel(k)                             # discard older records
+    layer.profile_enable(1)
+    for s in range(last, n_steps):
         step(s)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    t_end = time.perf_counter()
-    sweep_ms, sweep_launches = layer.profile_read()
-    sup_ms, sup_n = layer.profile_read_kernel("support")
-    act_ms, act_n = layer.profile_read_kernel("active")
+    layer.flush()
+    prof = {k: layer.profile_read_kernel(k) for k in ("sweep", "support", "active")}
+    layer.profile_read_kernel("structural")                      # any due inside the pass
+    for _ in range(STRUCTURAL_TIMED):
+        layer.structural_update(count=False)
+    su_ms, su_n = layer.profile_read_kernel("structural")
+    # the whole-matrix log-weight pass (recompute_weights), timed the same way
+    for _ in range(WEIGHT_PASSES):
+        layer.recompute_weights()
+    wp_ms, wp_n = layer.profile_read_kernel("weights")
     layer.profile_enable(0)
+    layer.close()
 
-    wall_s = t_end - t_start
-    gpu_s = ev0.elapsed_time(ev1) / 1e3
-    samples = sum(sched[s][3] for s in range(args.warmup, n_steps))
-    plastic_steps = sum(sched[s][4] for s in range(args.warmup, n_steps))
-    value = samples / wall_s
+    csrc = os.path.join(ROOT, "paper_2106_05373_amd", "csrc")
+    traffic_key = w.name if pairs else w.name + ":unpaired"
+    prof_samples = sum(sched[s][3] for s in range(last, n_steps))
+    avg_b = prof_samples / max(profile_steps, 1)
+    b_pad = 16 * ((B + 15) // 16)
+    active = k_act * L.in_mcu * L.n_out
+    E = L.n_in * L.n_out
 
     # ---- roofline of the dominant kernel: the silent-element sweep -------------------------
     # Per launch it must read every Pij and write those of silent blocks (4 + 4 bytes per silent
     # element, 4 per active one), and read the split operands of each batch it applies once
     # (bf16 hi and lo of x and t, 4 bytes per element per padded batch row; with complement
     # pairs x covers the first unit of each input HCU only, and the column sums of t per
-    # 16-row tile are read as well).  Its contractions run on bf16 matrix cores (three split
-    # products per batch).  It runs on the layer's second stream, one workgroup per CU for a
-    # small layer, overlapping the next batches' support and active-block kernels, so its
-    # duration is set by that sharing as much as by its traffic.
-    sizes = sweep_sizes(sched, args.warmup, n_steps)
+    # 16-row tile are read as well).
+    sizes = sweep_sizes(sched, last, n_steps)
+    # the library's choice of sweep: one workgroup per CU when the matrix has at most 64
+    # 32 x 32 blocks per CU, LDS-staged tiles otherwise
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    small_sweep = ((L.n_in + 31) // 32) * ((L.n_out + 31) // 32) <= 64 * n_cu
     per_sweep = sum(sizes) / len(sizes)
-    avg_b = samples / max(args.steps, 1)
-    b_pad = 16 * ((B + 15) // 16)
-    active = k_act * L.in_mcu * L.n_out
-    E = L.n_in * L.n_out
     pij_bytes = 4.0 * E + 4.0 * (E - active)
     n_x = L.in_hcu if pairs else L.n_in            # input units the contraction covers
     ops_bytes = 4.0 * (n_x + L.n_out) * b_pad + (4.0 * L.n_out * (b_pad // 16) if pairs else 0.0)
     bytes_per_launch = pij_bytes + per_sweep * ops_bytes
-    if sweep_launches == 0 or sweep_ms <= 0:
+    sweep_ms, sweep_n = prof["sweep"]
+    if sweep_n == 0 or sweep_ms <= 0:
         raise RuntimeError("no sweep launch was timed")
-    avg_sweep_s = sweep_ms / 1e3 / sweep_launches
+    avg_sweep_s = sweep_ms / 1e3 / sweep_n
     achieved_gbs = bytes_per_launch / avg_sweep_s / 1e9
-    flops_per_launch = 2.0 * n_x * L.n_out * avg_b * per_sweep
-    csrc = os.path.join(ROOT, "paper_2106_05373_amd", "csrc")
-    digest = source_digest(csrc)
-    traffic_key = args.workload if pairs else args.workload + ":unpaired"
-    traffic = MEASURED_TRAFFIC.get((traffic_key, digest))
+    traffic = MEASURED_TRAFFIC.get((traffic_key, kernel_digest(csrc, SWEEP_SOURCES)))
     roofline = {
         "bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS,
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
-        "kernel": "silent-block trace sweep (the x^T t contractions of up to "
-                  f"{SWEEP_BATCHES} consecutive batches on split-bf16 MFMA, one read and one write "
-                  "of Pij; a small layer: one workgroup per CU on a second stream overlapping "
-                  "later batches; a large layer: LDS-staged tiles on the caller's stream; "
-                  + ("trace_sweep_pair_kernel / trace_sweep_pair_tile_kernel: over the first "
-                     "unit of each (x, 1 - x) input pair, the second row from the column total)"
-                     if pairs else "trace_sweep_kernel / trace_sweep_tile_kernel)"),
-        "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_launches,
-        "timed_every": PROFILE_PERIOD if args.steps >= 32 * PROFILE_PERIOD else 1,
+        "kernel": ("trace_sweep_pair" if pairs else "trace_sweep") +
+                  ("_kernel" if small_sweep else "_tile_kernel") +
+                  " (silent-block trace sweep: one read and one write of Pij for up to "
+                  f"{SWEEP_BATCHES} queued batches, their x^T t contractions on split-bf16 MFMA; "
+                  + ("one workgroup per CU on the layer's second stream beside later batches)"
+                     if small_sweep else "128-row LDS-staged tiles on the caller's stream)"),
+        "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_n,
         "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
-        "contraction_tflops": round(flops_per_launch / avg_sweep_s / 1e12, 3),
+        "timing": "profiling pass after the timed region (every launch dispatch-stamped)",
+    }
+
+    # ---- the joint-trace contraction against the bf16 matrix cores it runs on --------------
+    # Algorithmic flops of X^T T over the units the sweep contracts (2 per multiply-add);
+    # executed: three split-bf16 products per multiply-add.
+    flops_alg = 2.0 * n_x * L.n_out * avg_b * per_sweep
+    contraction = {
+        "kernel": roofline["kernel"].split(" ")[0], "dtype": "bf16 (hi/lo split, 3 products)",
+        "algorithmic_tflops": round(flops_alg / avg_sweep_s / 1e12, 3),
+        "executed_tflops": round(3 * flops_alg / avg_sweep_s / 1e12, 3),
+        "peak": PEAK_BF16_MFMA_TFS, "unit": "TFLOP/s",
+        "frac_algorithmic": round(flops_alg / avg_sweep_s / 1e12 / PEAK_BF16_MFMA_TFS, 4),
     }
 
     # ---- the support GEMM on the fp64 matrix cores, and the caller's stream per batch --------
-    # Algorithmic flops of the masked support: 2 B A N_out, A = active input units per hidden
-    # HCU; both kernels are timed by their own dispatch events on the caller's stream.
+    sup_ms, sup_n = prof["support"]
+    act_ms, act_n = prof["active"]
     avg_sup_s = sup_ms / 1e3 / max(sup_n, 1)
     sup_flops = 2.0 * avg_b * k_act * L.in_mcu * L.n_out
     mfma = {
@@ -280,17 +378,19 @@ def main():
         "stream": "caller's: support then active-block trace kernel, every batch",
         "support_us": round(avg_sup_s * 1e6, 3),
         "active_us": round(act_ms / 1e3 / max(act_n, 1) * 1e6, 3),
-        "batch_us": round(wall_s * 1e6 / args.steps, 3),
+        "batch_us": round(wall_s * 1e6 / max(steps, 1), 3),
+    }
+    su_s = su_ms / 1e3 / max(su_n, 1)
+    structural_update = {
+        "kernels": "mi_kernel + swap_kernel", "avg_us": round(su_s * 1e6, 3),
+        "timed": su_n, "period_batches": w.period,
+        "amortized_us_per_batch": round(su_s * 1e6 / w.period, 3) if w.period else 0.0,
+        "in_timed_region": plastic_steps,
     }
 
-    # ---- the log-weight pass over the whole matrix (recompute_weights), after the timed run ---
+    # ---- the log-weight pass over the whole matrix (recompute_weights) ----------------------
     # Per launch it writes every w and reads the Pij of active blocks (a silent weight is 0
-    # whatever its trace), plus Pi, Pj and the mask.  Timed by its own dispatch events.
-    layer.profile_enable(1)
-    for _ in range(WEIGHT_PASSES):
-        layer.recompute_weights()
-    wp_ms, wp_n = layer.profile_read_kernel("weights")
-    layer.profile_enable(0)
+    # whatever its trace), plus Pi, Pj and the mask.
     wp_bytes = 4.0 * E + 4.0 * active + 4.0 * (L.n_in + L.n_out) + L.in_hcu * L.out_hcu
     wp_s = wp_ms / 1e3 / max(wp_n, 1)
     weight_pass = {
@@ -299,57 +399,32 @@ def main():
         "bound": "hbm", "achieved": round(wp_bytes / wp_s / 1e9, 1) if wp_n else None,
         "peak": PEAK_HBM_GBS, "unit": "GB/s",
         "frac": round(wp_bytes / wp_s / 1e9 / PEAK_HBM_GBS, 4) if wp_n else None,
-        "traffic": MEASURED_WEIGHT_TRAFFIC.get((traffic_key, digest)),
+        "traffic": MEASURED_WEIGHT_TRAFFIC.get((traffic_key,
+                                                kernel_digest(csrc, WEIGHT_SOURCES))),
         "algorithmic_bytes_per_launch": wp_bytes, "avg_us": round(wp_s * 1e6, 3),
         "timed_launches": wp_n,
     }
-
-    # ---- the two products at their dense size, against the fp32 matrix-core peak -------------
-    # What a dense fp32 implementation would run per batch: the support X (W o mask) and the
-    # contraction X^T Y over every element, 2 B N_in N_out flops each.  Here the support skips
-    # silent blocks (fp64) and the contraction runs as split bf16 (over half the rows with
-    # complement pairs), so these rates are dense-equivalent: the dense product's flops over
-    # the time the kernels take to deliver its result (support: its event-timed duration;
-    # contraction: the sweep's time per batch plus the active-block kernel's).
-    dense_flops = 2.0 * avg_b * L.n_in * L.n_out
-    act_s = act_ms / 1e3 / max(act_n, 1)
-    trace_s = avg_sweep_s / per_sweep + act_s
-    dense_equivalent = {
-        "unit": "TFLOP/s", "peak": PEAK_F32_MFMA_TFS, "flops_per_batch": dense_flops,
-        "support": round(dense_flops / avg_sup_s / 1e12, 2) if sup_n else None,
-        "support_frac": round(dense_flops / avg_sup_s / 1e12 / PEAK_F32_MFMA_TFS, 3)
-                        if sup_n else None,
-        "trace": round(dense_flops / trace_s / 1e12, 2),
-        "trace_frac": round(dense_flops / trace_s / 1e12 / PEAK_F32_MFMA_TFS, 3),
+    config = {
+        "workload": f"{w.name}: {n_train} synthetic images -> {L.in_hcu}x{L.in_mcu} inputs, "
+                    f"hidden {L.out_hcu} HCUs x {L.out_mcu} MCUs, "
+                    f"{int(round(w.mask_frac * 100))}% receptive fields, plasticity every "
+                    f"{w.period} batches, alpha {w.alpha}",
+        "global_batch": B, "samples_timed": samples, "structural_updates_timed": plastic_steps,
+        "wall_s": round(wall_s, 6), "support_accumulation": "f64",
+        "complement_pairs": bool(pairs), "data_staging_s": round(prep_s, 2),
+        "timed_region": "K steps then bcpnn_flush (every queued silent-block update of the "
+                        "timed batches applied), between two device synchronisations; no "
+                        "profiling events",
+        "launch": ("HIP graph: the K steps' library calls captured once before the timed "
+                   "region, replayed once inside it" if launch == "graph" else
+                   "eager: one library call per step inside the timed region"),
+        "other_launch": other_fig,
+        "parallelism": "single GPU",
     }
-
-    out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(wall_s * 1e3 / args.steps, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {
-            "workload": f"{w.name}: {w.n_train} synthetic images -> {L.in_hcu}x{L.in_mcu} inputs, "
-                        f"hidden {L.out_hcu} HCUs x {L.out_mcu} MCUs, "
-                        f"{int(round(w.mask_frac * 100))}% receptive fields, plasticity every "
-                        f"{w.period} batches, alpha {w.alpha}",
-            "global_batch": B, "samples_timed": samples, "structural_updates_timed": plastic_steps,
-            "gpu_event_s": round(gpu_s, 6), "wall_s": round(wall_s, 6),
-            "support_accumulation": "f64", "complement_pairs": bool(pairs),
-            "data_staging_s": round(prep_s, 2),
-            "parallelism": "single GPU",
-        },
-        "roofline": roofline,
-        "mfma": mfma,
-        "critical_path": critical_path,
-        "weight_pass": weight_pass,
-        "dense_equivalent": dense_equivalent,
-    }
-
-    if not args.no_cpu_baseline and args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(w, mask, shuffled, sched, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
-    layer.close()
+    return {"value": round(samples / wall_s, 1), "ms_per_step": round(wall_s * 1e3 / steps, 5),
+            "config": config, "roofline": roofline, "contraction": contraction, "mfma": mfma,
+            "critical_path": critical_path, "structural_update": structural_update,
+            "weight_pass": weight_pass, "mask": mask}
 
 
 def run_pipeline(args):
@@ -556,16 +631,17 @@ def run_precision_report(args):
         "oracle_wall_s": round(t_oracle, 1), "storage": rows}), flush=True)
 
 
-def run_inference_sweep(args):
-    """Forward-pass (support + softmax) throughput of the MNIST-shaped layer by batch size."""
+def run_inference_sweep():
+    """Forward-pass (support + softmax) throughput of the MNIST-shaped layer by batch size: one
+    launch per batch, timed over repeated launches between two synchronisations."""
     import torch
     from paper_2106_05373_amd import bcpnn, synth
 
     w = synth.WORKLOADS["mnist"]
     L = w.layer
-    sizes = [1, 8, 32, 128, 512, 2048, 8192]
+    sizes = INFERENCE_BATCHES
     dev = torch.device("cuda", 0)
-    px, _ = synth.dataset(w, n=max(sizes))
+    px, _ = synth.dataset(w, split="test", n=max(sizes))
     X = torch.from_numpy(synth.encode_pixels(px)).to(dev)
     mask = synth.random_mask(L.in_hcu, L.out_hcu, synth.active_count(L.in_hcu, w.mask_frac),
                              w.seed_mask)
@@ -587,42 +663,79 @@ def run_inference_sweep(args):
         rows.append({"batch": B, "us_per_batch": round(dt * 1e6, 2),
                      "samples_per_s": round(B / dt, 1)})
     layer.close()
-    print(json.dumps({"metric": "inference samples/s by batch size (support + per-HCU softmax)",
-                      "config": {"workload": f"mnist layer {L.in_hcu}x{L.in_mcu} -> "
-                                             f"{L.out_hcu}x{L.out_mcu}, 10% receptive fields"},
-                      "data": "synthetic", "dtype": "f32 (fp64 accumulation)",
-                      "sweep": rows}), flush=True)
+    return {"metric": "inference samples/s by batch size (support + per-HCU softmax)",
+            "config": {"workload": f"mnist layer {L.in_hcu}x{L.in_mcu} -> "
+                                   f"{L.out_hcu}x{L.out_mcu}, 10% receptive fields"},
+            "data": "synthetic", "dtype": "f32 (fp64 accumulation)", "sweep": rows}
 
 
-def cpu_baseline(w, mask, shuffled, sched, budget_s):
-    """The CPU oracle (as it stands) on the first batches of the same schedule, until the time
-    budget is spent; samples/s over the batches it finished."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, mask, budget_s, n_batches=200):
+    """The CPU oracle (as it stands) on this host's cores, on the MNIST-shaped schedule's first
+    batches (the same images, shuffle and mask as the GPU run; structural updates before the
+    100th and 200th).  All threads: the first n_batches batches, or as many as fit the budget.
+    One thread: as many batches as fit half the budget, plus one structural update timed on the
+    state they reach, amortised over its period."""
     import oracle
+    from paper_2106_05373_amd import synth
     L = w.layer
+    B = w.batch
+    sched = schedule(w.n_train, B, w.period, n_batches)
+    px, _ = synth.dataset(w)
+    Xe = synth.encode_pixels(px)[synth.epoch_permutation(w.n_train, w.seed_shuffle, 0)]
+    del px
     p = oracle.make_params(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, alpha=w.alpha, gain=w.gain,
-                           init_noise=w.init_noise, seed=w.seed_noise)
-    ora = oracle.OracleLayer(p, mask)
-    host = {e: None for e in shuffled}
-    for e in sorted(host)[:2]:                    # copies made before the clock starts
-        host[e] = shuffled[e].cpu().numpy()
-    done = samples = plastic = 0
-    t0 = time.perf_counter()
-    for (e, k, start, size, is_plastic) in sched:
-        if host[e] is None:
-            break
-        if is_plastic:
-            ora.structural_update()
-            plastic += 1
-        ora.train_batch(host[e][start:start + size])
-        done += 1
-        samples += size
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
-    return {"value": round(samples / el, 2), "unit": "samples/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": f"first {done} batches ({samples} samples, {plastic} structural updates) "
-                      f"of the same schedule in {el:.1f} s"}
+                           bias_gain=w.bias_gain, init_noise=w.init_noise, seed=w.seed_noise)
+    all_threads = oracle.threads()
+
+    def run(budget):
+        ora = oracle.OracleLayer(p, mask)
+        done = samples = plastic = 0
+        t0 = time.perf_counter()
+        for (e, k, start, size, is_plastic) in sched:
+            if is_plastic:
+                ora.structural_update()
+                plastic += 1
+            ora.train_batch(Xe[start:start + size])
+            done += 1
+            samples += size
+            if time.perf_counter() - t0 >= budget:
+                break
+        return ora, done, samples, plastic, time.perf_counter() - t0
+
+    _, done, samples, plastic, el = run(budget_s)
+    out = {"value": round(samples / el, 2), "unit": "samples/s", "cores": all_threads,
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": f"first {done} batches ({samples} samples, {plastic} structural updates, "
+                     f"period {w.period}) of the MNIST-shaped schedule in {el:.1f} s, "
+                     f"{all_threads} OpenMP threads"}
+    oracle.set_threads(1)
+    try:
+        ora, done1, samples1, plastic1, el1 = run(budget_s / 2)
+        t0 = time.perf_counter()
+        ora.structural_update()
+        su = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(all_threads)
+    per_batch = el1 / done1 + (su / w.period if plastic1 == 0 else 0.0)
+    out["single_thread"] = {
+        "value": round(B / per_batch, 2), "unit": "samples/s", "cores": 1,
+        "sample": f"first {done1} batches ({samples1} samples) in {el1:.1f} s, plus one "
+                  f"structural update timed on the state they reach ({su:.2f} s) amortised "
+                  f"over its period of {w.period} batches" if plastic1 == 0 else
+                  f"first {done1} batches ({samples1} samples, {plastic1} structural updates) "
+                  f"in {el1:.1f} s"}
+    return out
 
 
 if __name__ == "__main__":

@@ -29,22 +29,32 @@
  * Ownership and streams: the layer owns every state buffer (allocated in create, freed in
  * destroy).  Caller buffers named *_dev are device pointers (16-byte aligned, contiguous) that
  * the caller owns; *_host are host pointers.  Every call enqueues its kernels on the stream
- * given to create and returns without waiting, except get_state, set_state, get_mi and
- * structural_update with a non-NULL count pointer, which wait for the stream.  Calls on one
- * layer must not run concurrently from several host threads.
+ * given to create and returns without waiting, except get_state, set_state, get_mi, the
+ * profile reads and structural_update with a non-NULL count pointer, which wait for the
+ * stream.  Calls on one layer must not run concurrently from several host threads.
  *
  * Second stream: train_batch updates, on the caller's stream, everything the next batch reads
  * (Pij and w of active blocks, Pi, Pj, b, the activities).  The Pij of silent blocks are
  * updated on a stream the layer owns (default priority, non-blocking), for up to eight batches
  * in one pass with the same per-batch arithmetic; the caller's stream is made to wait for that
  * work before every call that reads or replaces Pij (get_state, set_state, structural_update,
- * recompute_weights, profile_read) and destroy waits for both streams.  The results are those
- * of per-batch updates, bit for bit.
+ * recompute_weights, the profile reads, flush) and destroy waits for both streams.  The results
+ * are those of per-batch updates, bit for bit.
+ *
+ * HIP graphs: forward, train_batch, recompute_weights, readout, flush and structural_update
+ * with a NULL count allocate nothing, wait for nothing and enqueue no memset, so a sequence of
+ * them can be captured on the layer's stream (with profiling off) into a HIP graph.  The
+ * layer's host-side bookkeeping (which trace and operand buffers the next batch uses, which
+ * silent updates are queued) advances when a call is made, so a captured sequence that ends
+ * with flush must be replayed exactly once, before any later call on the layer.
  *
  * Errors: every call returns a bcpnn_status.  Arguments are checked on the host before any
  * device work; BCPNN_EINVAL leaves the layer unchanged.  A failed HIP call returns
  * BCPNN_EDEVICE and marks the layer failed: later calls on it return BCPNN_ESTATE (destroy
- * still works).  bcpnn_last_error() describes the last failure of the calling thread.
+ * still works).  Input properties that only the device can see (complement_pairs below) are
+ * checked by the kernels and reported by the next call that waits for the stream, as
+ * BCPNN_EINPUT, which also marks the layer failed.  bcpnn_last_error() describes the last
+ * failure of the calling thread.
  */
 #ifndef BCPNN_H
 #define BCPNN_H
@@ -62,7 +72,10 @@ typedef enum {
     BCPNN_EINVAL = -1,   /* invalid argument; nothing was changed                        */
     BCPNN_ENOMEM = -2,   /* device or host allocation failed                             */
     BCPNN_EDEVICE = -3,  /* a HIP call failed; the layer is now unusable                 */
-    BCPNN_ESTATE = -4    /* the layer failed earlier                                     */
+    BCPNN_ESTATE = -4,   /* the layer failed earlier                                     */
+    BCPNN_EINPUT = -5    /* an earlier train_batch's input broke a property the layer was
+                            configured with (complement_pairs); its traces are not the
+                            method's; the layer is now unusable                          */
 } bcpnn_status;
 
 /* Storage format of Pij and W.  F32 stores fp32.  BF16 and M10 keep fp32 arrays whose values
@@ -99,9 +112,10 @@ typedef struct {
                                    of the second row of each pair is then taken as
                                    sum_b t_bj - sum_b x_b t_bj, equal in real arithmetic for
                                    such inputs, so the joint-trace contraction runs over half
-                                   the input units.  Inputs that are not complementary pairs
-                                   get that update all the same.  0 (the default) contracts
-                                   every input unit.                                          */
+                                   the input units.  train_batch checks every pair of its
+                                   input (|x_2p + x_2p+1 - 1| <= 1e-6, NaN fails) and a
+                                   violation makes the next waiting call return BCPNN_EINPUT.
+                                   0 (the default) contracts every input unit.                */
 } bcpnn_config;
 
 /* Host-side view of the layer state (fp32 arrays and the uint8 mask, layouts above). */
@@ -153,13 +167,24 @@ bcpnn_status bcpnn_recompute_weights(bcpnn_layer *layer);
  * n_swapped_host (nullable) receives the number of swaps; passing it waits for the stream. */
 bcpnn_status bcpnn_structural_update(bcpnn_layer *layer, int32_t *n_swapped_host);
 
-/* Readout: winner_dev [B][out_hcu] receives, for each sample and hidden HCU, the MCU index of
- * the largest support (ties: lowest index). */
+/* Readout (Sec. 2, inference: the trained network is evaluated like a conventional
+ * feed-forward network, from the support of the output layer): winner_dev [B][out_hcu]
+ * receives, for each sample and hidden HCU, the MCU index of the largest support s_j of the
+ * Alg. 1 support line (ties: lowest index).  No learning; 1 <= B <= max_batch.  x_dev as for
+ * forward; winner_dev is caller-owned device memory, 16-byte aligned. */
 bcpnn_status bcpnn_readout(bcpnn_layer *layer, const float *x_dev, int32_t B,
                            int32_t *winner_dev);
 
-/* Copies the state to host arrays (each pointer of the view may be NULL to skip it).  Waits. */
-bcpnn_status bcpnn_get_state(const bcpnn_layer *layer, const bcpnn_state_view *host_out);
+/* Applies the queued silent-block updates of Pij (train_batch defers them; see "Second stream"
+ * above) and makes the caller's stream wait for them: work enqueued on that stream after this
+ * call sees every Pij as per-batch updates leave it.  It enqueues only and does not wait for
+ * the host.  A caller that times a run, or hands the layer's stream to other work that reads
+ * Pij, calls it at the end of its batches.  Errors: ESTATE, EDEVICE. */
+bcpnn_status bcpnn_flush(bcpnn_layer *layer);
+
+/* Copies the state to host arrays (each pointer of the view may be NULL to skip it).  Applies
+ * the queued silent-block updates first (it enqueues work, so the layer is not const).  Waits. */
+bcpnn_status bcpnn_get_state(bcpnn_layer *layer, const bcpnn_state_view *host_out);
 
 /* Replaces the state from host arrays (all six pointers required).  The mask must satisfy the
  * create rules; w is stored with the mask applied (silent blocks become 0).  Waits. */
@@ -167,7 +192,7 @@ bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in
 
 /* Copies the mutual-information scores of the last structural update, [in_hcu][out_hcu] fp64,
  * to the host.  Waits.  EINVAL before the first structural update. */
-bcpnn_status bcpnn_get_mi(const bcpnn_layer *layer, double *mi_host);
+bcpnn_status bcpnn_get_mi(bcpnn_layer *layer, double *mi_host);
 
 /* Kernel timing for measurement: with period n > 0, every n-th launch of the silent-block sweep
  * of the joint traces (of the active-block trace kernel when the mask has no silent block),
@@ -182,15 +207,18 @@ bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);
 
 /* The same for one kernel: the silent-block sweep, the support (with softmax and the
- * contraction operands) or the active-block trace kernel of train_batch, or the weight pass of
- * recompute_weights (w over the whole matrix; the bias kernel after it is not included).
- * profile_enable's period applies to each kernel's own launch count.  Reads and clears that
- * kernel's record only.  Errors: EINVAL for an unknown kernel or NULL outputs. */
+ * contraction operands) or the active-block trace kernel of train_batch, the weight pass of
+ * recompute_weights (w over the whole matrix; the bias kernel after it is not included), or
+ * the structural update (from the start of the mutual-information kernel to the end of the
+ * swap kernel; the queued sweep it applies first is not included).  profile_enable's period
+ * applies to each kernel's own launch count.  Reads and clears that kernel's record only.
+ * Errors: EINVAL for an unknown kernel or NULL outputs. */
 typedef enum {
     BCPNN_KERNEL_SWEEP = 0,
     BCPNN_KERNEL_SUPPORT = 1,
     BCPNN_KERNEL_ACTIVE = 2,
-    BCPNN_KERNEL_WEIGHTS = 3
+    BCPNN_KERNEL_WEIGHTS = 3,
+    BCPNN_KERNEL_STRUCTURAL = 4
 } bcpnn_kernel;
 bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer *layer, int32_t kernel, double *total_ms,
                                        int32_t *launches);

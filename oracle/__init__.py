@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
         i32 = ctypes.c_int32
         sig = {
             "oracle_threads": (ctypes.c_int, []),
+            "oracle_set_threads": (None, [ctypes.c_int]),
             "oracle_round_storage": (ctypes.c_float, [ctypes.c_float, i32]),
             "oracle_splitmix_uniform": (ctypes.c_double, [ctypes.c_uint64, ctypes.c_uint64]),
             "oracle_init_state": (None, [P, u8, f32, f32, f32, f32, f32]),
@@ -108,6 +109,11 @@ def _i32(a):
 
 def threads() -> int:
     return int(lib().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of the oracle's loops from now on (results do not depend on it)."""
+    lib().oracle_set_threads(int(n))
 
 
 def splitmix_uniform(seed: int, idx: int) -> float:

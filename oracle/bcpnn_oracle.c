@@ -45,6 +45,14 @@ int oracle_threads(void) {
 #endif
 }
 
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------------------------
  * Storage rounding.  bf16 keeps 1 sign + 8 exponent + 7 mantissa bits of an fp32 value; the
  * "M10" format keeps 10 mantissa bits (the paper's BFn naming: n = 1 + 8 + mantissa, Sec. 3,

@@ -31,6 +31,8 @@ typedef struct {
 } oracle_params;
 
 int oracle_threads(void);
+/* Worker threads of the OpenMP loops from now on (n > 0); only timing depends on it. */
+void oracle_set_threads(int n);
 float oracle_round_storage(float v, int32_t storage);
 double oracle_splitmix_uniform(uint64_t seed, uint64_t idx);
 

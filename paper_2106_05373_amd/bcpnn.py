@@ -21,14 +21,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbcpnn.so")
 
 STORAGE = {"f32": 0, "bf16": 1, "m10": 2}
-KERNELS = {"sweep": 0, "support": 1, "active": 2, "weights": 3}
+KERNELS = {"sweep": 0, "support": 1, "active": 2, "weights": 3, "structural": 4}
 STATUS = {0: "BCPNN_OK", -1: "BCPNN_EINVAL", -2: "BCPNN_ENOMEM", -3: "BCPNN_EDEVICE",
-          -4: "BCPNN_ESTATE"}
+          -4: "BCPNN_ESTATE", -5: "BCPNN_EINPUT"}
 
 EXPORTS = [
     "bcpnn_config_default", "bcpnn_layer_create", "bcpnn_layer_destroy", "bcpnn_forward",
     "bcpnn_train_batch", "bcpnn_recompute_weights", "bcpnn_structural_update", "bcpnn_readout",
-    "bcpnn_get_state", "bcpnn_set_state", "bcpnn_get_mi", "bcpnn_profile_enable",
+    "bcpnn_flush", "bcpnn_get_state", "bcpnn_set_state", "bcpnn_get_mi", "bcpnn_profile_enable",
     "bcpnn_profile_read", "bcpnn_profile_read_kernel", "bcpnn_last_error",
 ]
 
@@ -73,6 +73,7 @@ def _load() -> ctypes.CDLL:
         "bcpnn_recompute_weights": (i32, [vp]),
         "bcpnn_structural_update": (i32, [vp, ctypes.POINTER(i32)]),
         "bcpnn_readout": (i32, [vp, vp, i32, vp]),
+        "bcpnn_flush": (i32, [vp]),
         "bcpnn_get_state": (i32, [vp, ctypes.POINTER(StateView)]),
         "bcpnn_set_state": (i32, [vp, ctypes.POINTER(StateView)]),
         "bcpnn_get_mi": (i32, [vp, vp]),
@@ -208,6 +209,10 @@ class Layer:
         _check(lib.bcpnn_readout(self._h, _dev_ptr(x, "x", torch.float32, (B, self.n_in)), B,
                                  _dev_ptr(winner, "winner", torch.int32, (B, self.cfg.out_hcu))))
 
+    def flush(self):
+        """Applies the queued silent-block updates of Pij on the layer's stream (no host wait)."""
+        _check(lib.bcpnn_flush(self._h))
+
     # -- state -----------------------------------------------------------------------------
     def get_state(self, which=("pi", "pj", "pij", "w", "b", "mask")) -> dict:
         shapes = dict(pi=(self.n_in,), pj=(self.n_out,), pij=(self.n_in, self.n_out),
@@ -249,7 +254,8 @@ class Layer:
         return float(ms.value), int(n.value)
 
     def profile_read_kernel(self, kernel: str):
-        """(total ms, launches) of one train_batch kernel ("sweep", "support", "active")."""
+        """(total ms, launches) of one kernel: "sweep", "support", "active" (train_batch),
+        "weights" (recompute_weights) or "structural" (MI + swap of structural_update)."""
         ms = ctypes.c_double()
         n = ctypes.c_int32()
         _check(lib.bcpnn_profile_read_kernel(self._h, KERNELS[kernel], ctypes.byref(ms),

@@ -56,6 +56,8 @@ struct bcpnn_layer {
     int32_t* act_count = nullptr;        // [out_hcu]
     int32_t* swap_count = nullptr;       // [out_hcu]
     double* mi = nullptr;                // [in_hcu][out_hcu]
+    int32_t* pair_error = nullptr;       // input check of complement pairs (device flag)
+    int32_t pair_error_host = 0;         // its copy, read with the waits of the waiting calls
     // Split batch operands of the joint-trace contraction, kSets sets used in turn.  The silent
     // elements of Pij take the updates of up to kMaxSweepBatches consecutive batches in one
     // sweep on the side stream, which reads those batches' sets while later batches proceed.
@@ -79,7 +81,7 @@ struct bcpnn_layer {
         size_t used = 0;
         int64_t launches = 0;
     };
-    KernelTimer timers[4];               // indexed by bcpnn_kernel
+    KernelTimer timers[5];               // indexed by bcpnn_kernel
 };
 
 #define HIP_TRY(layer, expr)                                                             \
@@ -160,7 +162,7 @@ const char* build_active_lists(const bcpnn_config& c, const uint8_t* mask,
 void free_layer(bcpnn_layer* L) {
     if (!L) return;
     void* bufs[] = {L->pi[0], L->pi[1], L->pj[0], L->pj[1], L->pij, L->w, L->b, L->mask,
-                    L->act_list, L->act_count, L->swap_count, L->mi};
+                    L->act_list, L->act_count, L->swap_count, L->mi, L->pair_error};
     for (void* p : bufs)
         if (p) (void)hipFree(p);
     for (int k = 0; k < kSets; ++k) {
@@ -262,6 +264,23 @@ hipError_t join_side(bcpnn_layer* L) {
     return e;
 }
 
+// Enqueues the read of the device's input check (complement pairs) ahead of a wait.
+hipError_t read_input_check(bcpnn_layer* L) {
+    if (!L->cfg.complement_pairs) return hipSuccess;
+    return hipMemcpyAsync(&L->pair_error_host, L->pair_error, sizeof(int32_t),
+                          hipMemcpyDeviceToHost, L->stream);
+}
+
+// After the wait: EINPUT (and the layer marked failed) if a training input broke the pair
+// property the layer was configured with.
+bcpnn_status input_check_result(bcpnn_layer* L) {
+    if (!L->pair_error_host) return BCPNN_OK;
+    L->failed = true;
+    return fail(BCPNN_EINPUT, "complement_pairs is set but a training batch held an input pair "
+                              "(x_2p, x_2p+1) that does not add up to 1: the joint traces of the "
+                              "second units are not those of the inputs");
+}
+
 bool mask_is_full(const bcpnn_config& c, const std::vector<int32_t>& count) {
     for (int32_t v : count)
         if (v != c.in_hcu) return false;
@@ -351,6 +370,8 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = dalloc(&L->act_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->swap_count, (size_t)cfg->out_hcu);
     if (e == hipSuccess) e = dalloc(&L->mi, hh);
+    if (e == hipSuccess) e = dalloc(&L->pair_error, 1);
+    if (e == hipSuccess) e = hipMemsetAsync(L->pair_error, 0, sizeof(int32_t), L->stream);
     // split operands in fragment order: 1 KiB per 32 units and 16 batch rows; the units past
     // the layer in the last block are never written and must read as zero
     const int32_t n_ks = (cfg->max_batch + 15) / 16;
@@ -360,6 +381,7 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     for (int k = 0; k < kSets; ++k) {
         bcpnn::TraceOperands& o = L->ops[k];
         o.n_ks = n_ks;
+        o.pair_error = L->pair_error;
         if (e == hipSuccess) e = dalloc(&o.x_hi, xf);
         if (e == hipSuccess) e = dalloc(&o.x_lo, xf);
         if (e == hipSuccess) e = dalloc(&o.t_hi, tf);
@@ -520,23 +542,30 @@ bcpnn_status bcpnn_recompute_weights(bcpnn_layer* L) {
 bcpnn_status bcpnn_structural_update(bcpnn_layer* L, int32_t* n_swapped_host) {
     if (bcpnn_status st = usable(L)) return st;
     HIP_TRY(L, join_side(L));
+    // timed span: the start of the MI kernel to the end of the swap kernel (or of MI alone)
+    hipEvent_t t0, t1;
+    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_STRUCTURAL, &t0, &t1));
+    const bool swaps = L->cfg.n_swaps > 0;
     HIP_TRY(L, bcpnn::launch_mutual_information(L->stream, L->g, L->pi[L->cur], L->pj[L->cur],
-                                                L->pij, L->cfg.eps, L->mi));
+                                                L->pij, L->cfg.eps, L->mi, t0));
+    if (t1 && !swaps) HIP_TRY(L, hipEventRecord(t1, L->stream));
     L->mi_valid = true;
-    if (L->cfg.n_swaps > 0)
+    if (swaps)
         HIP_TRY(L, bcpnn::launch_plasticity_swap(L->stream, L->g, L->mi, L->cfg.n_swaps,
                                                  L->pi[L->cur], L->pj[L->cur], L->pij,
                                                  L->cfg.eps, L->drop_bits, L->mask, L->w,
-                                                 L->act_list, L->act_count, L->swap_count));
+                                                 L->act_list, L->act_count, L->swap_count, t1));
     if (n_swapped_host) {
         *n_swapped_host = 0;
-        if (L->cfg.n_swaps > 0) {
-            std::vector<int32_t> c((size_t)L->cfg.out_hcu);
+        std::vector<int32_t> c((size_t)L->cfg.out_hcu);
+        if (swaps)
             HIP_TRY(L, hipMemcpyAsync(c.data(), L->swap_count, c.size() * sizeof(int32_t),
                                       hipMemcpyDeviceToHost, L->stream));
-            HIP_TRY(L, hipStreamSynchronize(L->stream));
+        HIP_TRY(L, read_input_check(L));
+        HIP_TRY(L, hipStreamSynchronize(L->stream));
+        if (bcpnn_status st = input_check_result(L)) return st;
+        if (swaps)
             for (int32_t v : c) *n_swapped_host += v;
-        }
     }
     return BCPNN_OK;
 }
@@ -553,8 +582,13 @@ bcpnn_status bcpnn_readout(bcpnn_layer* L, const float* x_dev, int32_t B, int32_
     return BCPNN_OK;
 }
 
-bcpnn_status bcpnn_get_state(const bcpnn_layer* Lc, const bcpnn_state_view* v) {
-    bcpnn_layer* L = const_cast<bcpnn_layer*>(Lc);
+bcpnn_status bcpnn_flush(bcpnn_layer* L) {
+    if (bcpnn_status st = usable(L)) return st;
+    HIP_TRY(L, join_side(L));
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_get_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     if (bcpnn_status st = usable(L)) return st;
     if (!v) return fail(BCPNN_EINVAL, "view is NULL");
     const Geometry& g = L->g;
@@ -570,8 +604,9 @@ bcpnn_status bcpnn_get_state(const bcpnn_layer* Lc, const bcpnn_state_view* v) {
     HIP_TRY(L, d2h(v->w, L->w, E * sizeof(float)));
     HIP_TRY(L, d2h(v->b, L->b, (size_t)g.n_out * sizeof(float)));
     HIP_TRY(L, d2h(v->mask, L->mask, hh));
+    HIP_TRY(L, read_input_check(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
-    return BCPNN_OK;
+    return input_check_result(L);
 }
 
 bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
@@ -586,6 +621,9 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     const size_t E = (size_t)g.n_in * (size_t)g.n_out;
     const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
     HIP_TRY(L, join_side(L));
+    HIP_TRY(L, read_input_check(L));
+    HIP_TRY(L, hipStreamSynchronize(L->stream));
+    if (bcpnn_status st = input_check_result(L)) return st;
     HIP_TRY(L, hipMemcpyAsync(L->pi[L->cur], v->pi, (size_t)g.n_in * sizeof(float),
                               hipMemcpyHostToDevice, L->stream));
     HIP_TRY(L, hipMemcpyAsync(L->pj[L->cur], v->pj, (size_t)g.n_out * sizeof(float),
@@ -607,15 +645,15 @@ bcpnn_status bcpnn_set_state(bcpnn_layer* L, const bcpnn_state_view* v) {
     return BCPNN_OK;
 }
 
-bcpnn_status bcpnn_get_mi(const bcpnn_layer* Lc, double* mi_host) {
-    bcpnn_layer* L = const_cast<bcpnn_layer*>(Lc);
+bcpnn_status bcpnn_get_mi(bcpnn_layer* L, double* mi_host) {
     if (bcpnn_status st = usable(L)) return st;
     if (!mi_host) return fail(BCPNN_EINVAL, "mi_host is NULL");
     if (!L->mi_valid) return fail(BCPNN_EINVAL, "no structural update since the state was set");
     const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
     HIP_TRY(L, hipMemcpyAsync(mi_host, L->mi, hh * sizeof(double), hipMemcpyDeviceToHost, L->stream));
+    HIP_TRY(L, read_input_check(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
-    return BCPNN_OK;
+    return input_check_result(L);
 }
 
 bcpnn_status bcpnn_profile_enable(bcpnn_layer* L, int32_t enable) {
@@ -630,10 +668,12 @@ bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer* L, int32_t kernel, double* t
                                        int32_t* launches) {
     if (bcpnn_status st = usable(L)) return st;
     if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
-    if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_WEIGHTS)
+    if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_STRUCTURAL)
         return fail(BCPNN_EINVAL, "unknown kernel %d", kernel);
     HIP_TRY(L, join_side(L));
+    HIP_TRY(L, read_input_check(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
+    if (bcpnn_status st = input_check_result(L)) return st;
     bcpnn_layer::KernelTimer& tm = L->timers[kernel];
     double sum = 0.0;
     for (size_t k = 0; k < tm.used; ++k) {

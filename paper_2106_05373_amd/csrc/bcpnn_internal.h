@@ -64,7 +64,12 @@ struct TraceOperands {
     float* t_sum;     // [ceil(B / 16)][n_out]
     int32_t n_ks;     // k-steps per unit block: ceil(max_batch / 16)
     int32_t paired;   // PairMode: with complement pairs, x^T over input HCUs (see above)
+    // With complement pairs: set to 1 by the support kernel when a pair of the batch input is
+    // not (x, 1 - x) (|x_2p + x_2p+1 - 1| > kPairTolerance, or NaN); never cleared on the device.
+    int32_t* pair_error;
 };
+
+constexpr float kPairTolerance = 1e-6f;
 
 // How the trace kernels treat the input units.  kPairsSplit is kPairs for a small layer: the
 // active-block kernel then runs each contraction twice, in two waves that store the first and
@@ -149,14 +154,17 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
                               hipEvent_t stop = nullptr);
 
 // Mutual information of every (input HCU, hidden HCU) block, fp64, [in_hcu][out_hcu].
+// start (nullable) is stamped when the kernel starts.
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
-                                     const float* pj, const float* pij, float eps, double* mi);
+                                     const float* pj, const float* pij, float eps, double* mi,
+                                     hipEvent_t start = nullptr);
 
 // Greedy swap per hidden HCU, patch of the swapped blocks of w, rebuild of the active lists.
+// stop (nullable) is stamped when the kernel ends.
 hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const double* mi,
                                   int32_t n_swaps, const float* pi, const float* pj,
                                   const float* pij, float eps, int drop_bits, uint8_t* mask,
                                   float* w, int32_t* act_list, int32_t* act_count,
-                                  int32_t* swap_count);
+                                  int32_t* swap_count, hipEvent_t stop = nullptr);
 
 }  // namespace bcpnn

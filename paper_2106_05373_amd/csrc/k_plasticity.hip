@@ -9,6 +9,8 @@
 // 1e-16 relative, far below the gaps between distinct scores.  Blocks holding identical data
 // (e.g. inputs that never change) get bit-identical scores because every block is reduced by
 // the same lane pattern wherever it sits, and such ties go to the lowest HCU index.
+#include <hip/hip_ext.h>
+
 #include <climits>
 
 #include "bcpnn_internal.h"
@@ -208,10 +210,12 @@ swap_kernel(Geometry g, const double* __restrict__ mi, int32_t n_swaps,
 }  // namespace
 
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
-                                     const float* pj, const float* pij, float eps, double* mi) {
+                                     const float* pj, const float* pij, float eps, double* mi,
+                                     hipEvent_t start) {
     const int64_t per_wg = (int64_t)(kThreads / 64) * (64 / kGroup);
     const int64_t blocks = ((int64_t)g.in_hcu * g.out_hcu + per_wg - 1) / per_wg;
-    mi_kernel<<<(unsigned)blocks, kThreads, 0, stream>>>(g, pi, pj, pij, eps, mi);
+    hipExtLaunchKernelGGL(mi_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, start,
+                          nullptr, 0, g, pi, pj, pij, eps, mi);
     return hipGetLastError();
 }
 
@@ -219,10 +223,11 @@ hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const d
                                   int32_t n_swaps, const float* pi, const float* pj,
                                   const float* pij, float eps, int drop_bits, uint8_t* mask,
                                   float* w, int32_t* act_list, int32_t* act_count,
-                                  int32_t* swap_count) {
+                                  int32_t* swap_count, hipEvent_t stop) {
     if (n_swaps > kMaxSwaps) return hipErrorInvalidValue;
-    swap_kernel<<<(unsigned)g.out_hcu, kThreads, (size_t)g.in_hcu, stream>>>(
-        g, mi, n_swaps, pi, pj, pij, eps, drop_bits, mask, w, act_list, act_count, swap_count);
+    hipExtLaunchKernelGGL(swap_kernel, dim3((unsigned)g.out_hcu), dim3(kThreads),
+                          (size_t)g.in_hcu, stream, nullptr, stop, 0, g, mi, n_swaps, pi, pj,
+                          pij, eps, drop_bits, mask, w, act_list, act_count, swap_count);
     return hipGetLastError();
 }
 

@@ -200,8 +200,9 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     // in passes of 64 columns (lane = column): wave w takes passes 7 - w, 15 - w, ...  A pass
     // reads each of the 16 rows with one coalesced load (clamped in bounds, zero past the batch
     // or the range); the first pass is fetched before the softmax so that its latency hides.
-    const int64_t c0 = (int64_t)hj * g.n_in / g.out_hcu;
-    const int64_t c1 = (int64_t)(hj + 1) * g.n_in / g.out_hcu;
+    // (whole input HCUs: with complement pairs both units of a pair fall in one pass)
+    const int64_t c0 = (int64_t)hj * g.in_hcu / g.out_hcu * g.in_mcu;
+    const int64_t c1 = (int64_t)(hj + 1) * g.in_hcu / g.out_hcu * g.in_mcu;
     const int rows = B - row0 < kRows ? B - row0 : kRows;
     const int rt = row0 / kRows;
     const int n_pass = (int)((c1 - c0 + 63) / 64);
@@ -216,6 +217,20 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             xcol[r] = x[(int64_t)rr * g.n_in + ic];
         }
     };
+    // With complement pairs every pair (x_2p, x_2p+1) of these rows must add up to 1.  The
+    // range starts at an even column and passes are 64 columns wide, so the partner of an even
+    // column is the next lane's column.  A violation sets the layer's flag.
+    auto check_pairs = [&](int p) {
+        const int64_t i = c0 + (int64_t)p * 64 + lane;
+        const bool first = i < c1 && (i & 1) == 0;
+        bool bad = false;
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+            const float nb = __shfl_down(xcol[r], 1, 64);
+            bad |= first && r < rows && !(fabsf(xcol[r] + nb - 1.0f) <= kPairTolerance);
+        }
+        if (bad) *ops.pair_error = 1;
+    };
     auto split_store = [&](int p) {
         const int64_t i = c0 + (int64_t)p * 64 + lane;
         float sum = 0.0f;
@@ -224,6 +239,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             xcol[r] = r < rows ? xcol[r] : 0.0f;
             sum += xcol[r];
         }
+        if (ops.paired) check_pairs(p);
         if (i < c1) {
             // with complement pairs only the first unit of each input HCU enters the
             // contraction, at the HCU's index; every unit keeps its column sum

@@ -105,5 +105,6 @@ def test_null_layer_calls_are_rejected(b):
     assert L.bcpnn_structural_update(None, None) == -1
     assert L.bcpnn_readout(None, None, 1, None) == -1
     assert L.bcpnn_get_mi(None, None) == -1
+    assert L.bcpnn_flush(None) == -1
     assert L.bcpnn_layer_create(None, None, None, None) == -1
     L.bcpnn_layer_destroy(None)

@@ -151,6 +151,66 @@ def test_tiled_sweep_on_a_ragged_large_layer(pairs):
     pair.close()
 
 
+def test_flush_enqueues_exactly_the_queued_sweep():
+    """bcpnn_flush applies the queued silent-block updates on the caller's stream: three
+    batches then a flush give one sweep launch, a second flush with nothing queued none, and the
+    state equals that of a run read after every batch (grouping stays invisible)."""
+    import torch
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:6]]
+    cfg = workload_config(MNIST, alpha=0.02)
+    lay = bcpnn().Layer(cfg, workload_mask(MNIST))
+    lay.profile_enable(1)
+    counts = []
+    for x in xs[:3]:
+        lay.train_batch(x)
+    lay.flush()
+    lay.flush()
+    torch.cuda.synchronize()
+    counts.append(lay.profile_read_kernel("sweep")[1])
+    for x in xs[3:]:
+        lay.train_batch(x)
+        lay.flush()
+    counts.append(lay.profile_read_kernel("sweep")[1])
+    lay.profile_enable(0)
+    st = lay.get_state()
+    lay.close()
+    assert counts == [1, 3], counts
+    ref = bcpnn().Layer(cfg, workload_mask(MNIST))
+    for x in xs:
+        ref.train_batch(x)
+    st_ref = ref.get_state()
+    ref.close()
+    for key in st_ref:
+        assert np.array_equal(st_ref[key].view(np.uint8), st[key].view(np.uint8)), key
+
+
+@pytest.mark.parametrize("pairs", [1, 0])
+def test_inputs_that_are_not_pairs_fail_loudly(pairs):
+    """With complement_pairs set, a training batch whose input units are not (x, 1 - x) pairs
+    is reported by the next waiting call as BCPNN_EINPUT, and the layer refuses further work
+    (BCPNN_ESTATE); true pairs pass, and a layer without the setting accepts any input."""
+    import torch
+    B = bcpnn()
+    cfg = workload_config(MNIST, complement_pairs=pairs)
+    good = torch.from_numpy(np.ascontiguousarray(_inputs()[0])).cuda()
+    bad = good.clone()
+    bad[5, 2 * 300 + 1] += 0.01                   # one pair of one row no longer adds up to 1
+    lay = B.Layer(cfg, workload_mask(MNIST))
+    lay.train_batch(good)
+    lay.get_state(("pi",))
+    lay.train_batch(bad)
+    if pairs:
+        with pytest.raises(B.BcpnnError) as ei:
+            lay.get_state(("pi",))
+        assert ei.value.status == -5, ei.value
+        with pytest.raises(B.BcpnnError) as ei:
+            lay.train_batch(good)
+        assert ei.value.status == -4
+    else:
+        lay.get_state(("pi",))
+    lay.close()
+
+
 def test_profile_records_each_kernel():
     """Dispatch-stamped timing of each train_batch kernel: with period 1, nine batches give nine
     support and nine active-block launches and two sweeps (eight batches, then the one the read
