@@ -41,12 +41,13 @@
  * recompute_weights, the profile reads, flush) and destroy waits for both streams.  The results
  * are those of per-batch updates, bit for bit.
  *
- * HIP graphs: forward, train_batch, recompute_weights, readout, flush and structural_update
- * with a NULL count allocate nothing, wait for nothing and enqueue no memset, so a sequence of
- * them can be captured on the layer's stream (with profiling off) into a HIP graph.  The
- * layer's host-side bookkeeping (which trace and operand buffers the next batch uses, which
- * silent updates are queued) advances when a call is made, so a captured sequence that ends
- * with flush must be replayed exactly once, before any later call on the layer.
+ * HIP graphs: forward, train_batch, recompute_weights, readout, flush, structural_update
+ * with a NULL count and structural_update_static allocate nothing, wait for nothing and
+ * enqueue no memset, so a sequence of them can be captured on the layer's stream (with
+ * profiling off) into a HIP graph.  The layer's host-side bookkeeping (which trace and
+ * operand buffers the next batch uses, which silent updates are queued) advances when a call
+ * is made, so a captured sequence that ends with flush must be replayed exactly once, before
+ * any later call on the layer.
  *
  * Errors: every call returns a bcpnn_status.  Arguments are checked on the host before any
  * device work; BCPNN_EINVAL leaves the layer unchanged.  A failed HIP call returns
@@ -166,6 +167,20 @@ bcpnn_status bcpnn_recompute_weights(bcpnn_layer *layer);
  * rewrites the changed blocks of w.  The caller schedules it (before a batch).
  * n_swapped_host (nullable) receives the number of swaps; passing it waits for the stream. */
 bcpnn_status bcpnn_structural_update(bcpnn_layer *layer, int32_t *n_swapped_host);
+
+/* For callers that cannot allocate memory or wait for the device (code under HIP graph capture,
+ * serving loops, harnesses that forbid allocation): bcpnn_structural_update without them.  It
+ * computes the same scores and makes the same swaps and weight patches with the same kernels,
+ * but keeps the scores and per-HCU swap counts in a static scratch array of the library (32 MiB
+ * of device memory per GPU, held until the process ends) instead of the layer's buffers, and
+ * writes the number of swaps to n_swapped_dev (a device int32, 4-byte aligned, nullable)
+ * instead of returning it on the host.  It calls no allocating routine and does not wait.
+ * Limit: in_hcu * out_hcu * 8 (rounded up to 256) + out_hcu * 4 bytes <= 32 MiB, else EINVAL
+ * (e.g. 27648 x 100 HCUs fit).  Every call on one GPU shares that array and leaves the last
+ * call's contents in it, so such calls on one GPU must not overlap (calls on one stream never
+ * do; calls on different streams race).  The scores are not kept: get_mi afterwards returns
+ * EINVAL.  Errors: EINVAL, ESTATE, EDEVICE. */
+bcpnn_status bcpnn_structural_update_static(bcpnn_layer *layer, int32_t *n_swapped_dev);
 
 /* Readout (Sec. 2, inference: the trained network is evaluated like a conventional
  * feed-forward network, from the support of the output layer): winner_dev [B][out_hcu]

@@ -27,9 +27,10 @@ STATUS = {0: "BCPNN_OK", -1: "BCPNN_EINVAL", -2: "BCPNN_ENOMEM", -3: "BCPNN_EDEV
 
 EXPORTS = [
     "bcpnn_config_default", "bcpnn_layer_create", "bcpnn_layer_destroy", "bcpnn_forward",
-    "bcpnn_train_batch", "bcpnn_recompute_weights", "bcpnn_structural_update", "bcpnn_readout",
-    "bcpnn_flush", "bcpnn_get_state", "bcpnn_set_state", "bcpnn_get_mi", "bcpnn_profile_enable",
-    "bcpnn_profile_read", "bcpnn_profile_read_kernel", "bcpnn_last_error",
+    "bcpnn_train_batch", "bcpnn_recompute_weights", "bcpnn_structural_update",
+    "bcpnn_structural_update_static", "bcpnn_readout", "bcpnn_flush", "bcpnn_get_state",
+    "bcpnn_set_state", "bcpnn_get_mi", "bcpnn_profile_enable", "bcpnn_profile_read",
+    "bcpnn_profile_read_kernel", "bcpnn_last_error",
 ]
 
 
@@ -74,6 +75,7 @@ def _load() -> ctypes.CDLL:
         "bcpnn_structural_update": (i32, [vp, ctypes.POINTER(i32)]),
         "bcpnn_readout": (i32, [vp, vp, i32, vp]),
         "bcpnn_flush": (i32, [vp]),
+        "bcpnn_structural_update_static": (i32, [vp, vp]),
         "bcpnn_get_state": (i32, [vp, ctypes.POINTER(StateView)]),
         "bcpnn_set_state": (i32, [vp, ctypes.POINTER(StateView)]),
         "bcpnn_get_mi": (i32, [vp, vp]),
@@ -202,6 +204,13 @@ class Layer:
         n = ctypes.c_int32()
         _check(lib.bcpnn_structural_update(self._h, ctypes.byref(n)))
         return int(n.value)
+
+    def structural_update_static(self, n_swapped=None):
+        """bcpnn_structural_update_static: the swap count goes to n_swapped (a CUDA int32
+        tensor of one element, or None); no allocation, no host wait."""
+        import torch
+        _check(lib.bcpnn_structural_update_static(
+            self._h, _dev_ptr(n_swapped, "n_swapped", torch.int32, (1,))))
 
     def readout(self, x, winner):
         import torch

@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -25,6 +26,34 @@ constexpr int kSets = 3 * bcpnn::kMaxSweepBatches;
 constexpr int64_t kSmallSweepBlocksPerCu = 64;
 
 thread_local std::string g_error;
+
+// Scratch of bcpnn_structural_update_static: the MI scores ([in_hcu][out_hcu] fp64) and the
+// per-hidden-HCU swap counts of the update in flight.  Each GPU the library runs on holds its
+// own copy until the process ends; every such call on a GPU shares it.  Host code uses the
+// device address resolved per device (static_scratch), never the array's name.
+constexpr size_t kStaticScratchBytes = 32u << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on device `dev`, which must be current; resolved once per
+// device.
+hipError_t static_scratch(int dev, void** out) {
+    *out = nullptr;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 bcpnn_status fail(bcpnn_status st, const char* fmt, ...) {
     char buf[512];
@@ -75,6 +104,7 @@ struct bcpnn_layer {
     int64_t sweep_wgs = 0;               // sweep launch: one workgroup per CU, or -1 (tiles)
     bool mi_valid = false;
     bool failed = false;
+    void* scratch = nullptr;             // this device's static scratch (resolved at create)
     int32_t profile_every = 0;           // 0: off; n: every n-th launch of a kernel carries events
     struct KernelTimer {                 // dispatch-stamped event pairs of one kernel
         std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
@@ -210,7 +240,7 @@ hipError_t wait_sweep(bcpnn_layer* L, int64_t seq);
 // written their operands.  join: the caller's stream is about to wait for it (a state access or
 // a structural update), so the sweep runs there, after every earlier sweep, over the whole
 // machine.
-hipError_t launch_pending_sweep(bcpnn_layer* L, bool join = false) {
+hipError_t launch_pending_sweep(bcpnn_layer* L, bool join = false, bool timed = true) {
     if (L->n_pend == 0) return hipSuccess;
     bcpnn::SweepArgs a{};
     for (int t = 0; t < L->n_pend; ++t) {
@@ -225,7 +255,7 @@ hipError_t launch_pending_sweep(bcpnn_layer* L, bool join = false) {
     a.mask = L->mask;
     a.drop_bits = L->drop_bits;
     hipEvent_t t0 = nullptr, t1 = nullptr;
-    hipError_t e = timer_events(L, BCPNN_KERNEL_SWEEP, &t0, &t1);
+    hipError_t e = timed ? timer_events(L, BCPNN_KERNEL_SWEEP, &t0, &t1) : hipSuccess;
     if (e != hipSuccess) return e;
     // A small layer's sweep overlaps the next batches on the side stream, one workgroup per CU.
     // A large layer's tiled sweep runs in order on the caller's stream: it fills the machine,
@@ -257,9 +287,9 @@ hipError_t wait_sweep(bcpnn_layer* L, int64_t seq) {
 }
 
 // Applies the pending silent updates and makes the caller's stream wait for the last sweep:
-// every Pij is then current in stream order.
-hipError_t join_side(bcpnn_layer* L) {
-    hipError_t e = launch_pending_sweep(L, true);
+// every Pij is then current in stream order.  timed = false never creates profiling events.
+hipError_t join_side(bcpnn_layer* L, bool timed = true) {
+    hipError_t e = launch_pending_sweep(L, true, timed);
     if (e == hipSuccess && L->n_sweeps > 0) e = wait_sweep(L, L->n_sweeps - 1);
     return e;
 }
@@ -408,6 +438,9 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     const int64_t blocks = ((g.n_in + 31) / 32) * ((g.n_out + 31) / 32);
     if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : -1;
+    // this device's static scratch, resolved here (the device is current) for the
+    // non-allocating structural update
+    if (e == hipSuccess) e = static_scratch(dev, &L->scratch);
     // complement pairs: a small layer's active-block kernel splits the rows of each pair over
     // two waves (it is bound by latency, not by its matrix work)
     const int pair_mode = !cfg->complement_pairs ? bcpnn::kUnpaired
@@ -567,6 +600,37 @@ bcpnn_status bcpnn_structural_update(bcpnn_layer* L, int32_t* n_swapped_host) {
         if (swaps)
             for (int32_t v : c) *n_swapped_host += v;
     }
+    return BCPNN_OK;
+}
+
+bcpnn_status bcpnn_structural_update_static(bcpnn_layer* L, int32_t* n_swapped_dev) {
+    if (bcpnn_status st = usable(L)) return st;
+    if (((uintptr_t)n_swapped_dev & 3u) != 0)
+        return fail(BCPNN_EINVAL, "n_swapped_dev must be 4-byte aligned");
+    const size_t hh = (size_t)L->cfg.in_hcu * L->cfg.out_hcu;
+    const size_t mi_bytes = (hh * sizeof(double) + 255) & ~(size_t)255;
+    const size_t need = mi_bytes + (size_t)L->cfg.out_hcu * sizeof(int32_t);
+    if (need > kStaticScratchBytes)
+        return fail(BCPNN_EINVAL,
+                    "structural_update_static needs %zu bytes of scratch (in_hcu * out_hcu * 8 + "
+                    "out_hcu * 4, rounded) but its static scratch holds %zu; use "
+                    "bcpnn_structural_update", need, kStaticScratchBytes);
+    if (!L->scratch) return fail(BCPNN_EDEVICE, "static scratch not resolved on this device");
+    double* mi = reinterpret_cast<double*>(L->scratch);
+    int32_t* counts = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(L->scratch) + mi_bytes);
+    HIP_TRY(L, join_side(L, false));
+    HIP_TRY(L, bcpnn::launch_mutual_information(L->stream, L->g, L->pi[L->cur], L->pj[L->cur],
+                                                L->pij, L->cfg.eps, mi));
+    if (L->cfg.n_swaps > 0)
+        HIP_TRY(L, bcpnn::launch_plasticity_swap(L->stream, L->g, mi, L->cfg.n_swaps,
+                                                 L->pi[L->cur], L->pj[L->cur], L->pij,
+                                                 L->cfg.eps, L->drop_bits, L->mask, L->w,
+                                                 L->act_list, L->act_count, counts));
+    if (n_swapped_dev)
+        HIP_TRY(L, bcpnn::launch_count_sum(L->stream, counts,
+                                           L->cfg.n_swaps > 0 ? L->cfg.out_hcu : 0,
+                                           n_swapped_dev));
+    L->mi_valid = false;                 // the scores stay in the shared scratch only
     return BCPNN_OK;
 }
 

@@ -167,4 +167,8 @@ hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const d
                                   float* w, int32_t* act_list, int32_t* act_count,
                                   int32_t* swap_count, hipEvent_t stop = nullptr);
 
+// total[0] = counts[0] + ... + counts[n - 1] (one workgroup; 0 for n = 0).
+hipError_t launch_count_sum(hipStream_t stream, const int32_t* counts, int32_t n,
+                            int32_t* total);
+
 }  // namespace bcpnn

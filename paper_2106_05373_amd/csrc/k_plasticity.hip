@@ -207,7 +207,29 @@ swap_kernel(Geometry g, const double* __restrict__ mi, int32_t n_swaps,
         if (mcol[h] == 1) list[pos++] = h;
 }
 
+// total[0] = sum of counts[0 .. n) (0 for n = 0), in one workgroup, in a fixed order.
+__global__ void __launch_bounds__(kThreads)
+count_sum_kernel(const int32_t* __restrict__ counts, int32_t n, int32_t* __restrict__ total) {
+    __shared__ int32_t part[kThreads / 64];
+    int32_t v = 0;
+    for (int32_t k = threadIdx.x; k < n; k += kThreads) v += counts[k];
+    v = wave_sum(v);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int32_t t = 0;
+        for (int q = 0; q < kThreads / 64; ++q) t += part[q];
+        total[0] = t;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_count_sum(hipStream_t stream, const int32_t* counts, int32_t n,
+                            int32_t* total) {
+    count_sum_kernel<<<1, kThreads, 0, stream>>>(counts, n, total);
+    return hipGetLastError();
+}
 
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
                                      const float* pj, const float* pij, float eps, double* mi,
