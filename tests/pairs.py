@@ -20,6 +20,19 @@ TOL_W = 1e-4            # weights and bias: |dw| <= TOL_W * max(1, |w|)
 TOL_W_STORAGE = {"f32": TOL_W, "bf16": 2.0 ** -7, "m10": 2.0 ** -10}
 TOL_S_REL = 1e-6        # support: fp64 sums on both sides, rounded to fp32 (<= a few ulp)
 TOL_MI_REL = 1e-12      # fp64 mutual information: summation order and libm differences
+# Trace increments from a common prior state (the change a step makes, not the value, so that
+# small learning rates are resolved).  A step is P <- c1 P + c2 T (c1 = 1 - alpha_eff); per
+# element, |dP_gpu - dP_oracle| <= TOL_INC_REL * |c2 T| + TOL_INC_ULPS fp32 ulps of the value,
+# with |c2 T| = |P_new - c1 P_old| from the oracle's states (summed over the steps of a run).
+# The relative part covers the split-bf16 contraction: each product carries at most about
+# 2^-16 of its value (the dropped lo*lo term and the rounding of the lo parts; all products are
+# non-negative, so the sum does too), and 1e-4 is 6.5 times that.  The ulps cover the rounding
+# of the stored result on both sides (half an ulp each) and the fp32 rounding of c1 (about half
+# an ulp of the value).
+TOL_INC_REL = 1e-4
+TOL_INC_ULPS = 4
+# Stored mantissa bits of the storage formats of Pij and w.
+STORAGE_BITS = {"f32": 23, "bf16": 7, "m10": 10}
 
 
 def bcpnn():
@@ -94,6 +107,15 @@ class Pair:
         s_o, y_o = self.ora.forward(x)
         return y.cpu().numpy(), s.cpu().numpy(), y_o, s_o
 
+    def forward_gpu_only(self, x):
+        """The GPU forward pass alone: (y, s, None, None)."""
+        t = self.torch
+        xd = self.dev(x)
+        y = t.empty((x.shape[0], self.n_out), device="cuda", dtype=t.float32)
+        s = t.empty_like(y)
+        self.gpu.forward(xd, y, s)
+        return y.cpu().numpy(), s.cpu().numpy(), None, None
+
     def close(self):
         self.gpu.close()
 
@@ -125,3 +147,94 @@ def assert_support_close(s_gpu, s_ora):
     small = np.abs(s_ora) < 1e-30
     assert np.all(err[~small] <= TOL_S_REL), f"support: max rel error {err[~small].max():.3g}"
     assert np.all(np.abs(s_gpu[small]) < 1e-30)
+
+
+def ulp(v, bits=23):
+    """Spacing of a binary floating-point format with `bits` stored mantissa bits at |v| (fp32:
+    23, bf16: 7, the 10-bit format: 10), with fp32's subnormal spacing as the floor."""
+    a = np.abs(np.asarray(v, np.float64))
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
+    return np.exp2(e - bits)
+
+
+def element_mask(block_mask, in_mcu, out_mcu):
+    """The (input HCU, hidden HCU) mask expanded to the [N_in][N_out] elements (True = active)."""
+    m = np.asarray(block_mask, bool)
+    return np.repeat(np.repeat(m, in_mcu, axis=0), out_mcu, axis=1)
+
+
+def decay(cfg):
+    """c1 = (1 - alpha)^n_cycles, the factor a step applies to the previous trace."""
+    return (1.0 - float(np.float32(cfg.alpha))) ** int(cfg.n_cycles)
+
+
+def assert_increments_close(prior, g, o, what, c1, ulps=TOL_INC_ULPS, select=None,
+                            resolved=0.5, contraction=None):
+    """The change from `prior` to the GPU's value `g` against the oracle's change to `o`:
+    |dg - do| <= TOL_INC_REL * |o - c1 prior| + ulps * ulp(value) for every element (of
+    `select`, a boolean mask of the elements to check).  For a run of several steps,
+    `contraction` replaces |o - c1 prior| by the sum of each step's |P_new - c1 P_old| on the
+    oracle side.  `resolved`: the fraction of the checked elements at which a 1% error in the
+    change would exceed the bound must reach it, else the case cannot tell a wrong update from a
+    right one."""
+    p = np.asarray(prior, np.float64).ravel()
+    gg = np.asarray(g, np.float64).ravel()
+    oo = np.asarray(o, np.float64).ravel()
+    ct = None if contraction is None else np.asarray(contraction, np.float64).ravel()
+    if select is not None:
+        sel = np.asarray(select, bool).ravel()
+        p, gg, oo = p[sel], gg[sel], oo[sel]
+        ct = None if ct is None else ct[sel]
+    if p.size == 0:
+        return
+    dg, do = gg - p, oo - p
+    if ct is None:
+        ct = np.abs(oo - c1 * p)
+    slack = ulps * ulp(np.maximum(np.abs(gg), np.abs(oo)))
+    bound = TOL_INC_REL * ct + slack
+    ratio = np.abs(dg - do) / bound
+    k = int(np.argmax(ratio))
+    frac = float(np.mean(0.01 * np.abs(do) > bound))
+    print(f"{what}: {p.size} elements, worst |d err| / bound {ratio[k]:.3g} "
+          f"(do {do[k]:.3g}, dg {dg[k]:.3g}), resolved at 1%: {frac:.3f}")
+    assert ratio[k] <= 1.0, (f"{what}: increment error {abs(dg[k] - do[k]):.3g} exceeds "
+                             f"{bound[k]:.3g} (oracle change {do[k]:.3g}, value {oo[k]:.3g})")
+    assert frac >= resolved, f"{what}: only {frac:.3f} of the changes are resolved at 1%"
+
+
+def pair_total(a):
+    """For a [N_in][N_out] array over complementary input pairs (x, 1 - x): each row replaced by
+    the sum of its pair's two rows.  With complement pairs the second row's contraction is the
+    column total minus the first's, so it carries the first row's absolute error: the error of
+    either row is relative to the pair's total."""
+    a = np.asarray(a, np.float64)
+    t = a.reshape(a.shape[0] // 2, 2, a.shape[1]).sum(axis=1)
+    return np.repeat(t, 2, axis=0)
+
+
+def assert_storage_close(g, o, storage, what, ulps=1, extra=0.0, scale=None):
+    """Values both sides round to a reduced storage format from fp32 results that agree to a
+    few fp32 ulps: at most `ulps` storage ulps apart (plus `extra` absolute), the ulp taken at
+    `scale` (default: the larger of the two values)."""
+    gg = np.asarray(g, np.float64)
+    oo = np.asarray(o, np.float64)
+    big = np.maximum(np.abs(gg), np.abs(oo))
+    if scale is not None:
+        big = np.maximum(big, np.asarray(scale, np.float64))
+    bound = ulps * ulp(big, STORAGE_BITS[storage]) + 4 * ulp(big) + extra
+    err = np.abs(gg - oo)
+    k = np.unravel_index(int(np.argmax(err - bound)), err.shape) if err.size else None
+    if k is not None:
+        assert err[k] <= bound[k], (f"{what}: {err[k]:.3g} apart at {k} (values {gg[k]:.6g}, "
+                                    f"{oo[k]:.6g}), more than {ulps} {storage} ulp")
+
+
+def assert_weights_storage_close(w_gpu, w_ora, storage, what="w"):
+    """Weights in a reduced storage format: the fp32 weight tolerance (the results before the
+    storage rounding) plus one storage ulp (the rounding may then land on neighbours)."""
+    wg = np.asarray(w_gpu, np.float64)
+    wo = np.asarray(w_ora, np.float64)
+    bound = TOL_W * np.maximum(1.0, np.abs(wo)) + ulp(np.maximum(np.abs(wg), np.abs(wo)),
+                                                      STORAGE_BITS[storage])
+    err = np.abs(wg - wo)
+    assert np.all(err <= bound), f"{what}: max excess {float(np.max(err - bound)):.3g}"

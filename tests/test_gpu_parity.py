@@ -12,9 +12,10 @@ import pytest
 import oracle
 from paper_2106_05373_amd import synth
 
-from pairs import (TOL_ACT, TOL_ACT_LOWP, TOL_MI_REL, Pair, assert_state_close,
-                   assert_support_close, assert_weights_close, gpu_config, max_abs,
-                   workload_config, workload_mask)
+from pairs import (TOL_ACT, TOL_ACT_LOWP, TOL_MI_REL, Pair, assert_increments_close,
+                   assert_state_close, assert_storage_close, assert_support_close,
+                   assert_weights_close, assert_weights_storage_close, element_mask, gpu_config,
+                   max_abs, workload_config, workload_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -69,6 +70,26 @@ def test_forward_matches_oracle(B):
     pair.close()
 
 
+@pytest.mark.parametrize("B", [512, 8192])
+def test_forward_at_inference_batch_sizes(B):
+    """The forward pass of the MNIST-shaped layer at the inference sweep's large batches (one
+    launch of B / 16 row tiles per hidden HCU) from a trained state: the support (fp64 sums on
+    both sides) and activities of 512 rows against the oracle -- all of them at B = 512, rows
+    sampled over the whole batch at B = 8192 (each row of the forward pass is independent)."""
+    w = MNIST
+    X, _ = encoded(w, 128 * 31)
+    Xb, _ = encoded(w, B, split="test")
+    pair = Pair(workload_config(w, max_batch=B), workload_mask(w))
+    pretrain(pair, X, 30, 128, alpha=0.05)
+    y, s, _, _ = pair.forward_gpu_only(Xb)
+    rows = np.arange(B) if B <= 512 else np.sort(
+        np.random.default_rng(B).choice(B, 512, replace=False))
+    s_o, y_o = pair.ora.forward(Xb[rows])
+    assert_support_close(s[rows], s_o)
+    assert max_abs(y[rows], y_o) <= TOL_ACT
+    pair.close()
+
+
 CASES = {
     # name: (workload, config overrides, batch, target?)
     "tiny": (TINY, {}, 32, False),
@@ -93,12 +114,44 @@ CASES = {
 }
 
 
+def check_step(prior, sg, so, cfg, storage, where, ulps=None, storage_ulps=1, paired=None):
+    """State after one step from `prior` on both sides.  fp32 storage: the changes of Pi, Pj and
+    Pij (silent and active blocks apart) to the increment bound (with complement pairs, the
+    contraction term of a pair's two rows together); reduced storage: Pij and w within one
+    storage ulp, Pi and Pj (kept in fp32) to the increment bound."""
+    from pairs import TOL_INC_ULPS, decay, pair_total
+    paired = bool(getattr(cfg, "complement_pairs", 0)) if paired is None else paired
+    ulps = TOL_INC_ULPS if ulps is None else ulps
+    c1 = decay(cfg)
+    assert np.array_equal(sg["mask"], so["mask"]), f"{where} mask differs"
+    for k in ("pi", "pj"):                     # (gain 0 leaves Pj unchanged: no resolution asked)
+        assert_increments_close(prior[k], sg[k], so[k], f"{where} {k}", c1, ulps=ulps,
+                                resolved=0.0)
+    act = element_mask(prior["mask"], cfg.in_mcu, cfg.out_mcu)
+    if storage == "f32":
+        ct = np.abs(so["pij"].astype(np.float64) - c1 * prior["pij"].astype(np.float64))
+        if paired:
+            ct = pair_total(ct)
+        for name, sel in (("silent", ~act), ("active", act)):
+            assert_increments_close(prior["pij"], sg["pij"], so["pij"], f"{where} pij {name}",
+                                    c1, ulps=ulps, select=sel, contraction=ct)
+        assert_weights_close(sg["w"], so["w"], f"{where} w")
+    else:
+        assert_storage_close(sg["pij"], so["pij"], storage, f"{where} pij", ulps=storage_ulps)
+        assert_weights_storage_close(sg["w"], so["w"], storage, f"{where} w")
+    assert_weights_close(sg["b"], so["b"], f"{where} b")
+
+
 @pytest.mark.parametrize("case", list(CASES))
 def test_one_step_matches_oracle(case):
+    """One training step from the oracle's state after 30 faster steps, at the workload's own
+    rate: activities to 1e-5, the change of every trace to the increment bound (silent and
+    active blocks apart) or, with reduced storage, Pij and w within one storage ulp."""
     w, over, B, supervised = CASES[case]
     X, labels = encoded(w, 40 * B + B)
     pair = Pair(workload_config(w, max_batch=max(B, w.batch), **over), workload_mask(w))
     pretrain(pair, X, 30, B, alpha=0.05)
+    prior = pair.ora.get_state()
     target = None
     if supervised:
         target = np.zeros((B, pair.n_out), np.float32)
@@ -110,8 +163,9 @@ def test_one_step_matches_oracle(case):
     storage = over.get("storage", "f32")
     tol = TOL_ACT_LOWP if storage != "f32" else TOL_ACT
     assert max_abs(y, y_o) <= TOL_ACT, f"y {max_abs(y, y_o)}"
-    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), tol=tol, where=case,
-                       storage=storage)
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    assert_state_close(sg, so, tol=tol, where=case, storage=storage)
+    check_step(prior, sg, so, pair.cfg, storage, case)
     pair.close()
 
 
@@ -365,10 +419,13 @@ def test_other_shapes_one_step(shape):
 def test_stl_shape_sampled(pairs):
     """The STL-shaped layer at full size (55296 x 10000 traces, 5% receptive fields, batch 256)
     in the launch configuration the benchmark uses (complement pairs; also without): one
-    structural update, one batch and the whole-matrix weight pass, checked on sampled outputs.  The oracle recomputes the sampled rows of the support and activities
-    from the GPU's prior weights, and the sampled blocks of the traces and weights from the
-    prior state restricted to the sampled input and hidden HCUs (the trace and weight updates
-    are elementwise given the batch, so a sub-problem reproduces them exactly)."""
+    structural update, one batch at the workload's rate and the whole-matrix weight pass, on six
+    sampled hidden HCUs.  Every step is defined per hidden HCU (the MI of its column of blocks,
+    its swap, its support and softmax, its columns of Pj, Pij and w) and Pi depends on the input
+    alone, so the oracle runs the exact sub-layer of all 27648 input HCUs and the six hidden
+    HCUs from the GPU's prior state, independently of the GPU: MI and the swapped masks of those
+    HCUs, all 256 rows of their activities, and the change of every one of their traces (silent
+    and active blocks apart) are compared."""
     w = synth.WORKLOADS["stl"]
     Lw = w.layer
     px, _ = synth.dataset(w, n=256)
@@ -379,62 +436,56 @@ def test_stl_shape_sampled(pairs):
     t = __import__("torch")
     layer = bcpnn().Layer(cfg, mask)
     xd = t.from_numpy(x).cuda()
-    # a few batches move the state away from its initial product form
+    # a few faster batches move the state away from its initial product form
+    fast = workload_config(w, complement_pairs=pairs, alpha=0.05)
+    warm = bcpnn().Layer(fast, mask)
     for _ in range(3):
-        layer.train_batch(xd)
+        warm.train_batch(xd)
+    layer.set_state(warm.get_state())
+    warm.close()
     prior = layer.get_state()
     n = layer.structural_update()
+    mi = layer.get_mi()
     after_swap = layer.get_state(("w", "mask"))
     y = t.empty((256, Lw.n_out), device="cuda")
     layer.train_batch(xd, None, y)
     post = layer.get_state()
     y = y.cpu().numpy()
-    rng = np.random.default_rng(7)
-
-    # structural update: MI of sampled blocks and the mask's per-HCU invariants
-    p_full = oracle_params_for(cfg)
     assert (after_swap["mask"].sum(0) == mask.sum(0)).all()
     assert n <= Lw.out_hcu
-    mi = layer.get_mi()
-    hi_s = rng.choice(Lw.in_hcu, 40, replace=False)
-    hj_s = rng.choice(Lw.out_hcu, 6, replace=False)
-    sub = sub_problem(prior, hi_s, hj_s, Lw)
-    mi_o = oracle.mutual_information(sub["p"], sub["pi"], sub["pj"], sub["pij"])
-    np.testing.assert_allclose(mi[np.ix_(hi_s, hj_s)], mi_o, rtol=TOL_MI_REL, atol=1e-15)
-    # activities of sampled rows: support recomputed from the post-swap weights
-    rows = rng.choice(256, 3, replace=False)
-    s_o = oracle.support(p_full, x[rows], after_swap["w"], prior["b"])
-    y_o = oracle.softmax(p_full, s_o)
-    assert max_abs(y[rows], y_o) <= TOL_ACT
-    # traces and weights of the sampled blocks
-    sub_post = sub_problem(post, hi_s, hj_s, Lw)
-    cols = sub["cols"]
-    pi, pj, pij = oracle.update_traces(sub["p"], x[:, sub["rows"]], y[:, cols], sub["pi"],
-                                       sub["pj"], sub["pij"])
-    assert max_abs(pij, sub_post["pij"]) <= TOL_ACT
-    assert max_abs(pi, sub_post["pi"]) <= TOL_ACT
-    m_sub = after_swap["mask"][np.ix_(hi_s, hj_s)]
-    w_o, _ = oracle.update_weights(sub["p"], m_sub, pi, pj, pij)
-    assert_weights_close(sub_post["w"], w_o)
+
+    rng = np.random.default_rng(7)
+    hj_s = np.sort(rng.choice(Lw.out_hcu, 6, replace=False))
+    cols = (hj_s[:, None] * Lw.out_mcu + np.arange(Lw.out_mcu)).ravel()
+    p_sub = oracle.Params(Lw.in_hcu, Lw.in_mcu, len(hj_s), Lw.out_mcu, cfg.alpha, cfg.n_cycles,
+                          cfg.gain, cfg.bias_gain, cfg.eps, cfg.pi_init, cfg.pj_init,
+                          cfg.init_noise, cfg.seed, cfg.n_swaps, cfg.storage)
+    sub = oracle.OracleLayer(p_sub, np.ascontiguousarray(prior["mask"][:, hj_s]))
+    sub_prior = dict(pi=prior["pi"], pj=prior["pj"][cols],
+                     pij=np.ascontiguousarray(prior["pij"][:, cols]),
+                     w=np.ascontiguousarray(prior["w"][:, cols]), b=prior["b"][cols],
+                     mask=np.ascontiguousarray(prior["mask"][:, hj_s]))
+    del prior
+    sub.set_state(sub_prior)
+    # structural update: scores and the swaps of the sampled hidden HCUs, bit for bit
+    n_sub, mi_sub, _ = sub.structural_update()
+    np.testing.assert_allclose(mi[:, hj_s], mi_sub, rtol=TOL_MI_REL, atol=1e-15)
+    assert np.array_equal(after_swap["mask"][:, hj_s], sub.mask)
+    assert_weights_close(after_swap["w"][:, cols], sub.w, "w after the swap")
+    # one batch: activities of every row, then the changes of the traces
+    swapped = sub.get_state()
+    _, y_o = sub.train_batch(x)
+    assert max_abs(y[:, cols], y_o) <= TOL_ACT, max_abs(y[:, cols], y_o)
+    sg = dict(pi=post["pi"], pj=post["pj"][cols], pij=np.ascontiguousarray(post["pij"][:, cols]),
+              w=np.ascontiguousarray(post["w"][:, cols]), b=post["b"][cols],
+              mask=np.ascontiguousarray(post["mask"][:, hj_s]))
+    so = sub.get_state()
+    assert_state_close(sg, so, where="stl")
+    check_step(swapped, sg, so, p_sub, "f32", "stl", paired=bool(pairs))
     # the whole-matrix weight pass (one row per workgroup at this size) on the same state
     layer.recompute_weights()
-    w_re = layer.get_state(("w",))["w"][np.ix_(sub["rows"], cols)]
-    w_ro, _ = oracle.update_weights(sub["p"], m_sub, sub_post["pi"], sub_post["pj"],
-                                    sub_post["pij"])
-    assert_weights_close(w_re, w_ro)
+    sub.recompute_weights()
+    w_re = layer.get_state(("w",))["w"][:, cols]
+    assert_weights_close(w_re, sub.w, "recomputed w")
     layer.close()
-
-
-def oracle_params_for(cfg):
-    from pairs import oracle_params
-    return oracle_params(cfg)
-
-
-def sub_problem(st, hi_s, hj_s, Lw):
-    """The state restricted to the given input and hidden HCUs, as an oracle sub-layer."""
-    rows = (hi_s[:, None] * Lw.in_mcu + np.arange(Lw.in_mcu)).ravel()
-    cols = (hj_s[:, None] * Lw.out_mcu + np.arange(Lw.out_mcu)).ravel()
-    p = oracle.make_params(len(hi_s), Lw.in_mcu, len(hj_s), Lw.out_mcu, alpha=1e-3)
-    return dict(p=p, rows=rows, cols=cols, pi=st["pi"][rows], pj=st["pj"][cols],
-                pij=np.ascontiguousarray(st["pij"][np.ix_(rows, cols)]),
-                w=np.ascontiguousarray(st["w"][np.ix_(rows, cols)]))
+    print(f"swaps: {n} in all, {n_sub} among the sampled hidden HCUs {hj_s.tolist()}")

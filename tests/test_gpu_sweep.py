@@ -12,7 +12,10 @@ import pytest
 
 from paper_2106_05373_amd import synth
 
-from pairs import TOL_ACT, Pair, assert_state_close, bcpnn, max_abs, workload_config, workload_mask
+from pairs import (TOL_ACT, TOL_ACT_LOWP, TOL_INC_ULPS, Pair, decay, assert_increments_close,
+                   assert_state_close, assert_storage_close, assert_weights_close,
+                   assert_weights_storage_close, bcpnn, element_mask, max_abs, workload_config,
+                   workload_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -61,26 +64,93 @@ def test_sweep_grouping_is_bitwise_invisible(pairs):
         assert np.array_equal(states[0][key].view(np.uint8), states[1][key].view(np.uint8)), key
 
 
+class Moved:
+    """Sum over the steps of a run of the oracle's per-step contraction term |P_new - c1 P_old|
+    of each trace (what the contraction error of each step is relative to)."""
+
+    def __init__(self, ora, c1):
+        self.ora, self.c1 = ora, c1
+        self.sum = {k: np.zeros(getattr(ora, k).shape, np.float64) for k in ("pi", "pj", "pij")}
+        self.peak = np.abs(ora.pij.astype(np.float64))      # largest |Pij| along the run
+
+    def before(self):
+        self.prev = {k: getattr(self.ora, k).astype(np.float64) for k in self.sum}
+
+    def after(self):
+        for k in self.sum:
+            self.sum[k] += np.abs(getattr(self.ora, k).astype(np.float64) - self.c1 * self.prev[k])
+        np.maximum(self.peak, np.abs(self.ora.pij), out=self.peak)
+
+
+def check_run(prior, sg, so, cfg, storage, where, n_batches, moved):
+    """End state of a run of n_batches from a common prior state.  Pi, Pj (fp32 in every
+    format) and, with fp32 storage, Pij (silent and active blocks apart): the change over the
+    run to the increment bound, its relative part taken on the sum of the oracle's per-step
+    contraction terms (with complement pairs, of the pair's two rows together) and its ulp
+    allowance that of one step per batch (the roundings of each step add up).  Reduced storage:
+    Pij within two storage ulps of the largest value the element reached (a one-ulp difference
+    left where a step's result sits at a rounding midpoint persists, decaying with c1, while
+    the value may fall into a smaller binade, where rounding can add up to one more of that
+    binade's ulps per crossing), and w against the oracle's weights from the GPU's own traces
+    (within one storage ulp and the fp32 weight tolerance)."""
+    import oracle
+    from pairs import oracle_params, pair_total
+    ulps = TOL_INC_ULPS * n_batches
+    assert np.array_equal(sg["mask"], so["mask"]), f"{where} mask differs"
+    for k in ("pi", "pj"):
+        assert_increments_close(prior[k], sg[k], so[k], f"{where} {k}", moved.c1, ulps=ulps,
+                                resolved=0.0, contraction=moved.sum[k])
+    act = element_mask(prior["mask"], cfg.in_mcu, cfg.out_mcu)
+    if storage == "f32":
+        ct = pair_total(moved.sum["pij"]) if cfg.complement_pairs else moved.sum["pij"]
+        for name, sel in (("silent", ~act), ("active", act)):
+            assert_increments_close(prior["pij"], sg["pij"], so["pij"], f"{where} pij {name}",
+                                    moved.c1, ulps=ulps, select=sel, contraction=ct)
+        assert_weights_close(sg["w"], so["w"], f"{where} w")
+        assert_weights_close(sg["b"], so["b"], f"{where} b")
+    else:
+        assert_storage_close(sg["pij"], so["pij"], storage, f"{where} pij", ulps=2,
+                             scale=moved.peak)
+        w_o, b_o = oracle.update_weights(oracle_params(cfg), sg["mask"], sg["pi"], sg["pj"],
+                                         sg["pij"])
+        assert_weights_storage_close(sg["w"], w_o, storage, f"{where} w from the GPU's traces")
+        assert_weights_close(sg["b"], b_o, f"{where} b")
+
+
+@pytest.mark.parametrize("storage", ["f32", "bf16", "m10"])
 @pytest.mark.parametrize("pairs", [1, 0])
-def test_multi_batch_run_matches_oracle(pairs):
+def test_multi_batch_run_matches_oracle(pairs, storage):
     """Target-clamped batches (the traces then depend on the inputs alone, with no feedback
-    through the weights), no re-synchronisation: after 20 batches the state agrees with the
-    oracle to the per-step tolerances; a forward pass mid-run does not disturb the sweeps."""
+    through the weights), no re-synchronisation: after 20 batches (two sweeps of eight, the
+    rest applied by the read) the change of every trace agrees with the oracle's, silent and
+    active blocks apart; a forward pass mid-run does not disturb the sweeps."""
     rng = np.random.default_rng(5)
-    pair = Pair(workload_config(MNIST, alpha=0.02, complement_pairs=pairs), workload_mask(MNIST))
+    pair = Pair(workload_config(MNIST, alpha=0.02, complement_pairs=pairs, storage=storage),
+                workload_mask(MNIST))
     cfg = pair.cfg
     t = pair.torch
+    prior = pair.ora.get_state()
+    moved = Moved(pair.ora, decay(cfg))
     for k, x in enumerate(_inputs()):
         win = rng.integers(0, cfg.out_mcu, size=(x.shape[0], cfg.out_hcu))
         target = np.zeros((x.shape[0], cfg.out_hcu, cfg.out_mcu), np.float32)
         np.put_along_axis(target, win[..., None], 1.0, axis=-1)
+        moved.before()
         pair.train(x, target.reshape(x.shape[0], -1))
+        moved.after()
         if k == 6:
+            # (with reduced storage the two runs' weights are storage ulps apart by now, so only
+            # the fp32 run's activities are compared; the call must not disturb the queue)
             y = t.empty((x.shape[0], pair.n_out), device="cuda", dtype=t.float32)
             pair.gpu.forward(pair.dev(x), y)
-            _, y_o = pair.ora.forward(x)
-            assert max_abs(y.cpu().numpy(), y_o) <= TOL_ACT
-    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where=f"after {len(SIZES)} batches")
+            if storage == "f32":
+                _, y_o = pair.ora.forward(x)
+                assert max_abs(y.cpu().numpy(), y_o) <= TOL_ACT
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    where = f"after {len(SIZES)} batches"
+    if storage == "f32":
+        assert_state_close(sg, so, where=where)
+    check_run(prior, sg, so, cfg, storage, where, len(SIZES), moved)
     pair.close()
 
 
@@ -129,25 +199,36 @@ def test_state_calls_between_batches_see_every_update():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("storage", ["f32", "bf16", "m10"])
 @pytest.mark.parametrize("pairs", [1, 0])
-def test_tiled_sweep_on_a_ragged_large_layer(pairs):
+def test_tiled_sweep_on_a_ragged_large_layer(pairs, storage):
     """A layer just past the size at which the library sweeps silent blocks in workgroup tiles
     (257 x 66 blocks of 32: ragged row and column tiles), ten target-clamped batches of mixed
-    size (one sweep of eight, two pending), against the oracle."""
+    size (one sweep of eight, two pending), against the oracle: the change of every trace
+    (silent and active blocks apart), or Pij and w within storage ulps (the tiled kernels of
+    the reduced formats)."""
     from pairs import gpu_config
     in_hcu, out_hcu, out_mcu = 4100, 21, 100
     rng = np.random.default_rng(11)
     mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0] for c in range(out_hcu)], 1)
-    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05, complement_pairs=pairs),
-                mask)
-    for B in (64, 64, 40, 64, 23, 64, 1, 64, 64, 50):
+    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05, complement_pairs=pairs,
+                           storage=storage), mask)
+    prior = pair.ora.get_state()
+    moved = Moved(pair.ora, decay(pair.cfg))
+    sizes = (64, 64, 40, 64, 23, 64, 1, 64, 64, 50)
+    for B in sizes:
         p = rng.random((B, in_hcu)).astype(np.float32)
         x = synth.encode_pixels(p)
         win = rng.integers(0, out_mcu, size=(B, out_hcu))
         target = np.zeros((B, out_hcu, out_mcu), np.float32)
         np.put_along_axis(target, win[..., None], 1.0, axis=-1)
+        moved.before()
         pair.train(x, target.reshape(B, -1))
-    assert_state_close(pair.gpu.get_state(), pair.ora.get_state(), where="tiled sweep")
+        moved.after()
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    if storage == "f32":
+        assert_state_close(sg, so, where="tiled sweep")
+    check_run(prior, sg, so, pair.cfg, storage, "tiled sweep", len(sizes), moved)
     pair.close()
 
 
