@@ -115,8 +115,10 @@ static double initial_pj(const oracle_params *p) {
     return p->pj_init > 0.0f ? (double)p->pj_init : 1.0 / (double)p->out_mcu;
 }
 
-/* Initial state (Sec. 2: the mask and connectivity start random; the traces start at the
- * uniform distribution of each HCU, the joint at the product of its marginals). */
+/* Initial state.  Sec. 2 says only that the connectivity (mask) starts random; it gives no
+ * initial trace values.  The reading taken here: the traces start at the uniform distribution
+ * of each HCU and the joint at the product of its marginals, and the weights as masked
+ * SplitMix64 noise (with traces in product form alone every weight would be 0 and stay 0). */
 void oracle_init_state(const oracle_params *p, const uint8_t *mask, float *pi, float *pj,
                        float *pij, float *w, float *b) {
     const int64_t n_in = (int64_t)p->in_hcu * p->in_mcu;

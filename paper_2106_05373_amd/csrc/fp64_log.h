@@ -1,5 +1,8 @@
 // Natural logarithm of a positive normal double, about one ulp from the correctly rounded value
-// (host and device, so that a host test can check it against the C library).
+// (host and device, so that a host test can check it against the C library).  The method is the
+// argument reduction and s = f / (2 + f) form of the public-domain fdlibm e_log.c (Sun
+// Microsystems, 1993), with its split of ln 2 into a 32-bit head and a tail; the polynomial here
+// is the plain atanh Taylor series, not fdlibm's minimax coefficients.
 //
 // x = 2^k m with m in [sqrt(1/2), sqrt(2)) and f = m - 1.  With s = f / (2 + f),
 //   log(1 + f) = log((1 + s) / (1 - s)) = 2 atanh(s) = 2 s + s R(z),   z = s^2,

@@ -5,7 +5,7 @@ input generation: images, their (x, 1-x) unit encoding, receptive-field masks, p
 shuffles, one-hot labels and the preset layer/workload descriptions.  It contains none of the
 method's arithmetic (no support, softmax, trace, weight or plasticity computation).
 
-The paper trains on MNIST (28x28 grey) and STL-10 (96x96x3 colour) (Sec. 5, Results); neither
+The paper trains on MNIST (28x28 grey) and STL-10 (96x96x3 colour) (Sec. 4, results); neither
 dataset is available here, so these generators reproduce the image shapes, value range [0, 1]
 and coarse statistics (sparse strokes on a dark background; smooth colour fields with oriented
 class textures) from fixed seeds.  Every array is float32, C-contiguous.
