@@ -26,6 +26,7 @@ threads, and one).
 from __future__ import annotations
 
 import argparse
+import faulthandler
 import hashlib
 import json
 import os
@@ -44,8 +45,8 @@ PEAK_BF16_MFMA_TFS = 2500.0
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
 # In the profiling pass after the timed region, every PROFILE_PERIOD-th launch of each kernel
-# carries dispatch-stamped events (each costs its stream a few microseconds).
-PROFILE_PERIOD = 4
+# carries dispatch-stamped events.
+PROFILE_PERIOD = 1
 # Launches of the whole-matrix weight pass timed after the training run.
 WEIGHT_PASSES = 20
 # Structural updates timed after the profiling pass.
@@ -143,7 +144,13 @@ def schedule(n_train, batch, period, n_steps):
     return out
 
 
+def stage(msg):
+    """A progress line on stderr (the JSON line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
+    faulthandler.enable()          # a native crash prints the Python stack of every thread
     args = parse()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (got --gpus {args.gpus}); the "
@@ -198,8 +205,10 @@ def main():
                       "roofline": r["roofline"], "critical_path": r["critical_path"],
                       "structural_update": r["structural_update"],
                       "weight_pass": r["weight_pass"]}
+        stage("inference sweep")
         out["inference_sweep"] = run_inference_sweep()["sweep"]
     if not args.no_cpu_baseline and args.cpu_seconds > 0 and args.workload == "mnist":
+        stage("CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(w, res["mask"], args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
@@ -216,7 +225,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     L = w.layer
     B = w.batch
     if profile_steps is None:
-        profile_steps = min(max(steps, 256), 1024)
+        profile_steps = min(max(steps, 64), 512)
     n_train = n_images if n_images is not None else w.n_train
     n_other = steps                  # the other launch mode, timed on the following steps
     n_steps = warmup + steps + n_other + profile_steps
@@ -224,6 +233,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     epochs = sorted({s[0] for s in sched})
 
     # ---- data staged on the device (not timed) -----------------------------------------
+    stage(f"{w.name}: staging {len(epochs)} epoch copies of the inputs ({n_steps} steps)")
     t0 = time.time()
     px, _ = synth.dataset(w, n=n_images)
     X = torch.from_numpy(synth.encode_pixels(px))
@@ -242,6 +252,8 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     cfg = bcpnn.default_config(L.in_hcu, L.in_mcu, L.out_hcu, L.out_mcu, B, alpha=w.alpha,
                                gain=w.gain, bias_gain=w.bias_gain, init_noise=w.init_noise,
                                seed=w.seed_noise, complement_pairs=pairs)
+    stage(f"{w.name}: layer {L.in_hcu}x{L.in_mcu} -> {L.out_hcu}x{L.out_mcu}, batch {B}, "
+          f"complement pairs {pairs}")
     layer = bcpnn.Layer(cfg, mask, stream=stream)
 
     def step(s):
@@ -280,10 +292,12 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         return time.perf_counter() - t_start
 
     first, last = warmup, warmup + steps
+    stage(f"{w.name}: {warmup} warm-up steps done; timing {steps} steps ({launch})")
     wall_s = timed(first, last, launch)
     samples = sum(sched[s][3] for s in range(first, last))
     plastic_steps = sum(sched[s][4] for s in range(first, last))
     other = "graph" if launch == "eager" else "eager"
+    stage(f"{w.name}: timing the next {n_other} steps ({other})")
     el = timed(last, last + n_other, other)
     other_fig = {"launch": other,
                  "value": round(sum(sched[s][3] for s in range(last, last + n_other)) / el, 1),
@@ -293,6 +307,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
 
     # ---- untimed profiling pass: the following steps, every profile_period-th launch of each
     # kernel dispatch-stamped (sampled, so that the stream keeps the schedule's pace) --------
+    stage(f"{w.name}: profiling pass of {profile_steps} steps")
     for k in bcpnn.KERNELS:
         layer.profile_read_kernel(k)                             # discard older records
     layer.profile_enable(profile_period)
@@ -302,6 +317,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     prof = {k: layer.profile_read_kernel(k) for k in ("sweep", "support", "active")}
     layer.profile_read_kernel("structural")                      # any due inside the pass
     layer.profile_enable(1)
+    stage(f"{w.name}: structural updates and weight passes")
     for _ in range(STRUCTURAL_TIMED):
         layer.structural_update(count=False)
     su_ms, su_n = layer.profile_read_kernel("structural")
