@@ -56,12 +56,19 @@ INFERENCE_BATCHES = [1, 8, 32, 128, 512, 2048, 8192]
 # STL-shaped leg of the default line: warm-up and timed batches (the first images of the set).
 STL_WARMUP, STL_STEPS = 2, 16
 
-# HBM traffic per launch (bytes) of the sweep kernel and of the weight pass, from rocprofv3
-# FETCH_SIZE and WRITE_SIZE runs scaled by the copy-kernel calibration factors, keyed by
-# workload and the SHA-256 of the sources of that kernel (kernel_digest).  A changed source
-# reports null until measured again.
-MEASURED_WEIGHT_TRAFFIC = {}
-MEASURED_TRAFFIC = {}
+# Memory traffic per launch (bytes between the L2 caches and the memory side: HBM and the
+# Infinity Cache) of the sweep kernel and of the weight pass, from rocprofv3 counter runs:
+# 128 TCC_EA0_RDREQ_128B + 64 TCC_EA0_RDREQ_64B + 32 TCC_EA0_RDREQ_32B read, and
+# 64 TCC_EA0_WRREQ_64B + 32 (TCC_EA0_WRREQ - TCC_EA0_WRREQ_64B) written, per dispatch (a
+# plain 256 MiB device copy reads exactly 256 MiB and writes 256 MiB by these formulas, so no
+# scale factor applies).  Keyed by workload and the SHA-256 of the kernel's sources
+# (kernel_digest); a changed source reports null until measured again.  The sweep's figure
+# is for the counter run's average launch (MNIST shape: 7.65 batches per launch; STL shape:
+# 5.56), the weight pass's for every launch.
+_SWEEP_DIGEST = "964e0ca49fa72633a6276329dad1a26fc69d5c6628545419a3062567c55e0036"
+_WEIGHT_DIGEST = "480df61bf1362da48e521896e1fa4e810cbd73a2ee1e1aff7f24211d282d19af"
+MEASURED_TRAFFIC = {("mnist", _SWEEP_DIGEST): 92.91e6, ("stl", _SWEEP_DIGEST): 9337.53e6}
+MEASURED_WEIGHT_TRAFFIC = {("mnist", _WEIGHT_DIGEST): 21.77e6, ("stl", _WEIGHT_DIGEST): 2404.27e6}
 
 
 def kernel_digest(csrc, files):
