@@ -47,6 +47,7 @@ SWEEP_BATCHES = 8
 # In the profiling pass after the timed region, every PROFILE_PERIOD-th launch of each kernel
 # carries dispatch-stamped events.
 PROFILE_PERIOD = 1
+PROFILE_SYNC = 64
 # Launches of the whole-matrix weight pass timed after the training run.
 WEIGHT_PASSES = 20
 # Structural updates timed after the profiling pass.
@@ -320,6 +321,11 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     layer.profile_enable(profile_period)
     for s in range(last, n_steps):
         step(s)
+        # a device wait every PROFILE_SYNC steps bounds the dispatch-stamped launches in
+        # flight (the runtime has aborted with thousands of them queued); the queued sweeps
+        # are left alone, so the schedule stays that of the timed run
+        if (s - last) % PROFILE_SYNC == PROFILE_SYNC - 1:
+            torch.cuda.synchronize()
     layer.flush()
     prof = {k: layer.profile_read_kernel(k) for k in ("sweep", "support", "active")}
     layer.profile_read_kernel("structural")                      # any due inside the pass
