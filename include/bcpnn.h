@@ -39,7 +39,10 @@
  * in one pass with the same per-batch arithmetic; the caller's stream is made to wait for that
  * work before every call that reads or replaces Pij (get_state, set_state, structural_update,
  * recompute_weights, the profile reads, flush) and destroy waits for both streams.  The results
- * are those of per-batch updates, bit for bit.
+ * are those of per-batch updates, bit for bit, except on a large layer (more than 64 blocks of
+ * 32 x 32 elements per compute unit) with complement pairs and fp32 storage: there the silent
+ * elements take the queued updates regrouped as c1^n P + (the batches' scaled contractions),
+ * equal in real arithmetic and within a few fp32 ulps per batch of per-batch updates.
  *
  * HIP graphs: forward, train_batch, recompute_weights, readout, flush, structural_update
  * with a NULL count and structural_update_static allocate nothing, wait for nothing and

@@ -341,6 +341,8 @@ constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) 
 
 constexpr int kTileKC = 2;
 constexpr int kPairTileCB = 3;   // column blocks per workgroup of the tiled sweep with pairs
+constexpr int kSumTileCB = 8;    // column blocks per workgroup of the sum-form sweep
+constexpr int kSumTileWaves = 4; // waves (blocks of 32 input HCUs) per workgroup of it
 
 template <int kDropBits, int kKC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -940,6 +942,213 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     }
 }
 
+// The same sweep for fp32 storage, in sum form.  With no rounding to a storage format between
+// batches, the n queued updates P <- c1_t P + c2_t T_t of an element combine exactly (in real
+// arithmetic) into
+//   P_n = (c1_0 ... c1_{n-1}) P_0 + R,   R_t = c1_t R_{t-1} + c2_t T_t,
+// and for the second unit of a pair into (c1_0 ... c1_{n-1}) P2_0 + Stot - R with
+// Stot = sum_t (c1_{t+1} ... c1_{n-1}) c2_t S_t (S_t the column total).  The matrix cores
+// accumulate R / c2_t in place (the accumulator is scaled by c1_t c2_{t-1} / c2_t before batch
+// t's products), so the old traces are read only in the epilogue, and the registers they take
+// in trace_sweep_pair_tile_kernel hold more accumulators instead: a wave covers 32 kCB columns
+// (kCB = 8 against 3) with the same operand pipeline (one chunk in flight), so that each round
+// trip to memory feeds 8 / 3 times the matrix-core work.  kTW waves share the t items.
+// Measured on the STL-shaped layer (6.67 batches per launch, each variant beside the previous
+// one on one box): 4.16 ms per launch per-batch (trace_sweep_pair_tile_kernel), 3.49 ms with
+// kCB = 6, 3.33 ms with kCB = 8; 8 waves of kCB = 6 (256 input HCUs) 3.84 ms.  The result differs from per-batch updates by the
+// fp32 rounding of the regrouped sums (a few ulps per batch), not by more.
+template <int kKC, int kCB, int kTW>
+__global__ void __launch_bounds__(kTW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
+    constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
+    constexpr int kPerWave = kItems / kTW;
+    static_assert(kPerWave * kTW == kItems, "t items split evenly over the waves");
+    __shared__ u32x4 stage[2][kItems][64];
+    __shared__ float stot[32 * kCB];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n_out = (int)g.n_out;
+    const int n_pb = (g.in_hcu + 31) / 32, n_cb = (n_out + 31) / 32;
+    const int n_ti = (n_pb + kTW - 1) / kTW;
+    constexpr int kSweepTiles = kSweepRows / kTW;
+    const int wg = (int)xcd_linear_index(blockIdx.x, gridDim.x);
+    const int sweep = wg / (kSweepTiles * n_tj);
+    const int in_sweep = wg % (kSweepTiles * n_tj);
+    const int here = n_ti - sweep * kSweepTiles < kSweepTiles ? n_ti - sweep * kSweepTiles
+                                                              : kSweepTiles;
+    const int ti = sweep * kSweepTiles + in_sweep % here;
+    const int tj = in_sweep / here;
+    const int n_ks = a.n_ks;
+
+    const int bi = kTW * ti + wave;
+    const int bic = bi < n_pb ? bi : n_pb - 1;
+    const int p0 = bic * 32;
+    const int prs = g.in_hcu - p0 < 32 ? g.in_hcu - p0 : 32;
+    const bool live = bi < n_pb;                           // wave-uniform
+    const int j00 = kCB * tj * 32;
+    const int jl = lane & 31, il0 = 4 * (lane >> 5);
+
+    int n_ch = 0;
+    for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
+    // requests of the chunk at (batch t, first k-step k0), as in trace_sweep_pair_tile_kernel
+    u32x4 xc[kKC][2], xn[kKC][2];
+    auto request = [&](int t, int k0, int sb) {
+        const SweepBatch bt = a.bt[t];
+#pragma unroll
+        for (int q = 0; q < kPerWave; ++q) {
+            const int item = wave + kTW * q;
+            const int half = item & 1, cb = (item >> 1) % kCB, kq = item / (2 * kCB);
+            int blk = kCB * tj + cb;
+            blk = blk < n_cb ? blk : n_cb - 1;
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
+                                  (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
+            __builtin_amdgcn_global_load_lds((const void*)src,
+                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+        }
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
+            const int64_t fa = (((int64_t)bic * n_ks + ks) * 64 + lane) * 8;
+            xn[kq][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa);
+            xn[kq][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa);
+        }
+    };
+    auto next = [&](int& t, int& k0) {
+        k0 += kKC;
+        if (k0 >= a.bt[t].nk) { k0 = 0; ++t; }
+    };
+
+    int dt = 0, dk = 0;
+    request(dt, dk, 0);
+    next(dt, dk);
+
+    // Stot of the workgroup's 32 kCB columns (clamped), batch by batch in order
+    for (int cl = threadIdx.x; cl < 32 * kCB; cl += kTW * 64) {
+        const int col = j00 + cl < n_out ? j00 + cl : n_out - 1;
+        float v = 0.0f;
+        for (int t = 0; t < a.n_batches; ++t) {
+            const SweepBatch bt = a.bt[t];
+            MarginalIn m;
+#pragma unroll
+            for (int q = 0; q < kSums; ++q)
+                m.part[q] = bt.t_sum[(int64_t)(q < bt.nk ? q : bt.nk - 1) * n_out + col];
+            v = fmaf(bt.c2, marginal_colsum(m, bt.t_sum, n_out, col, bt.nk), v * bt.c1);
+        }
+        stot[cl] = v;
+    }
+
+    f16v acc[kCB];
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) acc[c] = f16v{};
+    int ct = 0, ck = 0;
+    for (int lc = 0; lc < n_ch; ++lc) {
+        // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
+        // items visible to every wave and tells that every wave is done with the other buffer
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            xc[kq][0] = xn[kq][0];
+            xc[kq][1] = xn[kq][1];
+        }
+        stage_barrier();
+        if (lc + 1 < n_ch) {
+            request(dt, dk, (lc + 1) & 1);
+            next(dt, dk);
+        }
+        const int sb = lc & 1;
+        if (ck == 0 && ct > 0) {
+            // batch ct starts: acc holds R_{ct-1} / c2_{ct-1}; make it R_{ct-1} c1_ct / c2_ct
+            const float sc = a.bt[ct].c1 * (a.bt[ct - 1].c2 / a.bt[ct].c2);
+#pragma unroll
+            for (int c = 0; c < kCB; ++c)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[c][r] *= sc;
+        }
+        const int nk = a.bt[ct].nk;
+#pragma unroll
+        for (int kq = 0; kq < kKC; ++kq) {
+            if (ck + kq < nk) {
+                const bf8 ah = __builtin_bit_cast(bf8, xc[kq][0]);
+                const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
+#pragma unroll
+                for (int c = 0; c < kCB; ++c) {
+                    const bf8 bh = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2][lane]);
+                    const bf8 bl = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[c], 0, 0, 0);
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[c], 0, 0, 0);
+                    acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[c], 0, 0, 0);
+                }
+            }
+        }
+        next(ct, ck);
+    }
+    stage_barrier();                                    // stot is visible to every wave
+
+    // ---- epilogue: P_n = c1^n P_0 + R, P2_n = c1^n P2_0 + Stot - R, silent elements; column
+    // block by column block -----------------------------------------------------------------
+    const rsrc_t rp = make_rsrc(a.pij + (int64_t)(2 * p0) * n_out, (uint32_t)(2 * prs) * n_out * 4u);
+    const uint32_t o0 = ((uint32_t)(2 * il0) * n_out + j00 + jl) * 4u;
+    const uint32_t odd = (uint32_t)n_out * 4u;
+    // byte offset of the lane's element of result register r in the first column block (row
+    // and column in the vector offset, so that the buffer's range check drops the rows past
+    // the layer and the columns past the last); column block c adds 128 c bytes (an immediate)
+    uint32_t rowoff[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) rowoff[r] = o0 + (uint32_t)(2 * (8 * (r >> 2) + (r & 3))) * odd;
+    float c1n = 1.0f;
+    for (int t = 0; t < a.n_batches; ++t) c1n *= a.bt[t].c1;
+    const float c2n = a.bt[a.n_batches - 1].c2;
+    // old traces of column block c, both rows of each pair (requested one pass ahead)
+    float pold[2][2][16];
+    auto request_old = [&](int c, int slot) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t off = rowoff[r] + 128u * c;
+            pold[slot][0][r] =
+                __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off, 0, 0));
+            pold[slot][1][r] =
+                __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rp, off + odd, 0, 0));
+        }
+    };
+    uint32_t act_bits[kCB];
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) {
+        const int j0 = j00 + 32 * c;
+        const int jc = j0 < n_out ? j0 : (n_cb - 1) * 32;
+        const int cols = n_out - jc < 32 ? n_out - jc : 32;
+        const int hu = lane < 32 ? p0 + (lane < prs ? lane : prs - 1)
+                                 : (jc + (lane - 32 < cols ? lane - 32 : cols - 1)) / g.out_mcu;
+        act_bits[c] = block_mask_bits_hu(g, a.mask, hu, lane);
+    }
+    request_old(0, 0);
+#pragma unroll
+    for (int c = 0; c < kCB; ++c) {
+        if (c + 1 < kCB) request_old(c + 1, (c + 1) & 1);
+        const int j0 = j00 + 32 * c;
+        if (live) {                                             // wave-uniform
+            const bool jok = j0 + jl < n_out;
+            const float st = stot[32 * c + jl];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int il = il0 + 8 * (r >> 2) + (r & 3);
+                const float R = c2n * acc[c][r];
+                const float pe = fmaf(c1n, pold[c & 1][0][r], R);
+                const float po = fmaf(c1n, pold[c & 1][1][r], st - R);
+                const uint32_t off = rowoff[r] + 128u * c;
+                const bool keep = jok && !((act_bits[c] >> il) & 1u);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pe), rp, keep ? off : kDrop,
+                                                      0, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(po), rp,
+                                                      keep ? off + odd : kDrop, 0, 0);
+            }
+        }
+        // (a compiler fence: block c + 2's loads, into this block's registers, stay after
+        // this block's stores)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    }
+}
+
 // Active blocks with complement pairs: trace_active_kernel with the block rows taken as 32 of
 // the hidden HCU's active input HCUs (64 rows), their first units gathered through the active
 // list.  kSplit (small layers, where the kernel is bound by latency rather than by its matrix
@@ -1134,17 +1343,23 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
     const int64_t n_cb = (g.n_out + 31) / 32;
     const int64_t n_cg = (n_cb + kWaves - 1) / kWaves;
     if (resident_wgs < 0 && a.paired) {
-        // large layer: 128 input HCUs x 64 columns per workgroup
+        // large layer: 128 input HCUs x 96 columns per workgroup; in the sum form (fp32
+        // storage) 128 x 256
         void (*kernel)(Geometry, SweepArgs, int) = nullptr;
+        int cbs = kPairTileCB, tw = kWaves;
         switch (a.drop_bits) {
-            case 0: kernel = trace_sweep_pair_tile_kernel<0, kTileKC, kPairTileCB>; break;
+            case 0:
+                kernel = trace_sweep_pair_tile_sum_kernel<kTileKC, kSumTileCB, kSumTileWaves>;
+                cbs = kSumTileCB;
+                tw = kSumTileWaves;
+                break;
             case 13: kernel = trace_sweep_pair_tile_kernel<13, kTileKC, kPairTileCB>; break;
             case 16: kernel = trace_sweep_pair_tile_kernel<16, kTileKC, kPairTileCB>; break;
             default: return hipErrorInvalidValue;
         }
-        const int64_t n_ti = (n_rb + 3) / 4;
-        const int64_t n_tj = (n_cb + kPairTileCB - 1) / kPairTileCB;
-        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(kWaves * 64), 0, stream,
+        const int64_t n_ti = (n_rb + tw - 1) / tw;
+        const int64_t n_tj = (n_cb + cbs - 1) / cbs;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(tw * 64), 0, stream,
                               start, stop, 0, g, a, (int)n_tj);
         return hipGetLastError();
     }

@@ -232,6 +232,42 @@ def test_tiled_sweep_on_a_ragged_large_layer(pairs, storage):
     pair.close()
 
 
+def test_large_layer_sum_form_grouping():
+    """A large layer with complement pairs and fp32 storage sweeps its silent blocks in sum
+    form (the queued batches' updates regrouped as c1^n P + R): the same batches run freely
+    (one sweep of eight, then two) and with the state read after every batch (ten sweeps of
+    one) give bitwise the same Pi, Pj, w, b, mask and active-block Pij, and silent-block Pij
+    within TOL_INC_ULPS fp32 ulps per batch of each other."""
+    import torch
+    from pairs import gpu_config, ulp
+    in_hcu, out_hcu, out_mcu = 4100, 21, 100
+    rng = np.random.default_rng(5)
+    mask = np.stack([synth.random_mask(in_hcu, 1, 104, 90 + c)[:, 0] for c in range(out_hcu)], 1)
+    cfg = gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05, complement_pairs=1)
+    sizes = (64, 64, 40, 64, 23, 64, 1, 64, 64, 50)
+    xs = [torch.from_numpy(synth.encode_pixels(rng.random((B, in_hcu)).astype(np.float32))).cuda()
+          for B in sizes]
+    states = []
+    for read_each in (False, True):
+        lay = bcpnn().Layer(cfg, mask)
+        for x in xs:
+            lay.train_batch(x)
+            if read_each:
+                lay.get_state(("pij",))
+        states.append(lay.get_state())
+        lay.close()
+    a, b = states
+    for key in ("pi", "pj", "w", "b", "mask"):
+        assert np.array_equal(a[key].view(np.uint8), b[key].view(np.uint8)), key
+    act = element_mask(a["mask"], 2, out_mcu)
+    assert np.array_equal(a["pij"][act].view(np.uint32), b["pij"][act].view(np.uint32))
+    silent = ~act
+    d = np.abs(a["pij"][silent].astype(np.float64) - b["pij"][silent])
+    scale = ulp(np.maximum(np.abs(a["pij"][silent]), np.abs(b["pij"][silent])))
+    worst = float(np.max(d / scale))
+    assert worst <= TOL_INC_ULPS * len(sizes), worst
+
+
 def test_flush_enqueues_exactly_the_queued_sweep():
     """bcpnn_flush applies the queued silent-block updates on the caller's stream: three
     batches then a flush give one sweep launch, a second flush with nothing queued none, and the
