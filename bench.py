@@ -14,8 +14,8 @@ queues and applies a few batches at a time) are inside it, and no kernel in it c
 profiling events.
 
 After the timed region, an untimed profiling pass continues the same schedule with every
-kernel launch stamped by HIP events (dispatch-stamped, so each brackets one kernel on its own
-stream); the kernel durations of the JSON line come from it: the roofline position of the
+kernel launch bracketed by HIP events recorded on its stream right before and after it; the
+kernel durations of the JSON line come from it: the roofline position of the
 dominant kernel (the sweep over the silent elements of Pij), the support and active-block
 kernels of the caller's stream, and the structural update.  The line also carries the
 whole-matrix weight pass, the STL-shaped layer (a short run of the same schedule on the first
@@ -45,9 +45,9 @@ PEAK_BF16_MFMA_TFS = 2500.0
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
 # In the profiling pass after the timed region, every PROFILE_PERIOD-th launch of each kernel
-# carries dispatch-stamped events.
+# is bracketed by events.
 PROFILE_PERIOD = 1
-PROFILE_SYNC = 64
+PROFILE_SYNC = 64             # steps of the profiling pass between two reads of the timers
 # Launches of the whole-matrix weight pass timed after the training run.
 WEIGHT_PASSES = 20
 # Structural updates timed after the profiling pass.
@@ -225,7 +225,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
                      launch="eager", profile_period=PROFILE_PERIOD):
     """Trains the workload's layer on its schedule: `warmup` untimed steps, `steps` timed
     between two synchronisations (ending with bcpnn_flush), then an untimed profiling pass of
-    the following steps with every kernel dispatch-stamped, structural updates and weight
+    the following steps with every kernel launch timed by events, structural updates and weight
     passes timed the same way.  Returns the fields of the JSON line."""
     import torch
     from paper_2106_05373_amd import bcpnn, synth
@@ -314,20 +314,27 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     last += n_other
 
     # ---- untimed profiling pass: the following steps, every profile_period-th launch of each
-    # kernel dispatch-stamped (sampled, so that the stream keeps the schedule's pace) --------
+    # kernel bracketed by events (sampled, so that the stream keeps the schedule's pace) -----
     stage(f"{w.name}: profiling pass of {profile_steps} steps")
     for k in bcpnn.KERNELS:
         layer.profile_read_kernel(k)                             # discard older records
     layer.profile_enable(profile_period)
+    prof = {k: (0.0, 0) for k in ("sweep", "support", "active")}
+
+    def collect():
+        # reading waits for the stream and returns the layer's event pairs for reuse: every
+        # PROFILE_SYNC steps, so that few timed launches are queued and few event
+        # pairs exist at any time (the runtime has aborted with thousands of both)
+        for k in prof:
+            ms, n = layer.profile_read_kernel(k)
+            prof[k] = (prof[k][0] + ms, prof[k][1] + n)
+
     for s in range(last, n_steps):
         step(s)
-        # a device wait every PROFILE_SYNC steps bounds the dispatch-stamped launches in
-        # flight (the runtime has aborted with thousands of them queued); the queued sweeps
-        # are left alone, so the schedule stays that of the timed run
         if (s - last) % PROFILE_SYNC == PROFILE_SYNC - 1:
-            torch.cuda.synchronize()
+            collect()
     layer.flush()
-    prof = {k: layer.profile_read_kernel(k) for k in ("sweep", "support", "active")}
+    collect()
     layer.profile_read_kernel("structural")                      # any due inside the pass
     layer.profile_enable(1)
     stage(f"{w.name}: structural updates and weight passes")
@@ -384,7 +391,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
         "timing": f"profiling pass of {profile_steps} steps after the timed region, every "
-                  f"{profile_period}th launch of each kernel dispatch-stamped",
+                  f"{profile_period}th launch of each kernel bracketed by events",
     }
 
     # ---- the joint-trace contraction against the bf16 matrix cores it runs on --------------

@@ -214,12 +214,14 @@ bcpnn_status bcpnn_get_mi(bcpnn_layer *layer, double *mi_host);
 
 /* Kernel timing for measurement: with period n > 0, every n-th launch of the silent-block sweep
  * of the joint traces (of the active-block trace kernel when the mask has no silent block),
- * counting from the call, carries a pair of HIP events stamped by the dispatch itself
- * (hipExtLaunchKernel), so they bracket the kernel's execution alone; n = 0 turns it off.  Each
- * timed launch costs the stream a few microseconds of dispatch, so a period of 10 or more
- * keeps a throughput measurement nearly unperturbed.  bcpnn_profile_read applies the pending
- * silent updates, waits for both streams and returns the summed duration (ms) and count of the
- * timed launches since the last read.
+ * counting from the call, is bracketed by a pair of HIP events recorded on its stream right
+ * before and after it (their interval is the kernel's execution plus the events' short passage
+ * through the stream); n = 0 turns it off.  Each timed launch costs the stream a few
+ * microseconds, so a period of 10 or more keeps a throughput measurement nearly
+ * unperturbed.  bcpnn_profile_read waits for both
+ * streams and returns the summed duration (ms) and count of the timed launches since the last
+ * read; silent updates still queued stay queued (a read does not change which batches a sweep
+ * covers: bcpnn_flush applies them).
  * Errors: EINVAL for n < 0. */
 bcpnn_status bcpnn_profile_enable(bcpnn_layer *layer, int32_t period);
 bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *launches);

@@ -106,7 +106,7 @@ struct bcpnn_layer {
     bool failed = false;
     void* scratch = nullptr;             // this device's static scratch (resolved at create)
     int32_t profile_every = 0;           // 0: off; n: every n-th launch of a kernel carries events
-    struct KernelTimer {                 // dispatch-stamped event pairs of one kernel
+    struct KernelTimer {                 // event pairs around the timed launches of one kernel
         std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
         size_t used = 0;
         int64_t launches = 0;
@@ -734,9 +734,11 @@ bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer* L, int32_t kernel, double* t
     if (!total_ms || !launches) return fail(BCPNN_EINVAL, "total_ms and launches are required");
     if (kernel < BCPNN_KERNEL_SWEEP || kernel > BCPNN_KERNEL_STRUCTURAL)
         return fail(BCPNN_EINVAL, "unknown kernel %d", kernel);
-    HIP_TRY(L, join_side(L));
+    // every launch so far complete on both streams; queued silent updates stay queued, so
+    // that reading the timers leaves the schedule of the sweeps as it is
     HIP_TRY(L, read_input_check(L));
     HIP_TRY(L, hipStreamSynchronize(L->stream));
+    HIP_TRY(L, hipStreamSynchronize(L->side));
     if (bcpnn_status st = input_check_result(L)) return st;
     bcpnn_layer::KernelTimer& tm = L->timers[kernel];
     double sum = 0.0;

@@ -21,6 +21,22 @@ inline int storage_drop_bits(int32_t storage) {
 
 // ---- launchers (each enqueues on `stream` and returns hipGetLastError()) ----
 
+// Launches kernel<<<grid, block, lds, stream>>>(args...), with start / stop (each nullable)
+// recorded on the stream right before and after it: the elapsed time between them is the
+// kernel's, with the event records' own short passage through the stream.
+template <typename... Params, typename... Args>
+hipError_t launch_timed(void (*kernel)(Params...), dim3 grid, dim3 block, size_t lds,
+                        hipStream_t stream, hipEvent_t start, hipEvent_t stop, Args&&... args) {
+    if (start) {
+        const hipError_t e = hipEventRecord(start, stream);
+        if (e != hipSuccess) return e;
+    }
+    kernel<<<grid, block, lds, stream>>>(static_cast<Args&&>(args)...);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && stop) e = hipEventRecord(stop, stream);
+    return e;
+}
+
 // Initial state: Pij = pij0, w = mask ? noise * (2u - 1) : 0 with u from SplitMix64.
 hipError_t launch_init_state(hipStream_t stream, const Geometry& g, const uint8_t* mask,
                              float pij0, float init_noise, uint64_t seed, int drop_bits,
@@ -126,7 +142,7 @@ int64_t trace_active_workgroups(const Geometry& g, int32_t max_active, int paire
 // The elements of silent blocks over several consecutive batches: each element is read once,
 // takes the batches' updates Pij <- c1 Pij + c2 T in order (rounded to the storage format after
 // each, exactly as per-batch updates), and is written once.  Reads the mask; Pi, Pj, w and b
-// are untouched.  start / stop (nullable) receive the kernel's own start and end time stamps.
+// are untouched.  start / stop (nullable) are recorded on the stream around the launch.
 constexpr int kMaxSweepBatches = 8;
 struct SweepBatch {
     const uint16_t* x_hi;
@@ -154,13 +170,13 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
                               hipEvent_t stop = nullptr);
 
 // Mutual information of every (input HCU, hidden HCU) block, fp64, [in_hcu][out_hcu].
-// start (nullable) is stamped when the kernel starts.
+// start (nullable) is recorded on the stream right before the launch.
 hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, const float* pi,
                                      const float* pj, const float* pij, float eps, double* mi,
                                      hipEvent_t start = nullptr);
 
 // Greedy swap per hidden HCU, patch of the swapped blocks of w, rebuild of the active lists.
-// stop (nullable) is stamped when the kernel ends.
+// stop (nullable) is recorded on the stream right after the launch.
 hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const double* mi,
                                   int32_t n_swaps, const float* pi, const float* pj,
                                   const float* pij, float eps, int drop_bits, uint8_t* mask,

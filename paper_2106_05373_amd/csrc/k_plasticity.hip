@@ -9,8 +9,6 @@
 // 1e-16 relative, far below the gaps between distinct scores.  Blocks holding identical data
 // (e.g. inputs that never change) get bit-identical scores because every block is reduced by
 // the same lane pattern wherever it sits, and such ties go to the lowest HCU index.
-#include <hip/hip_ext.h>
-
 #include <climits>
 
 #include "bcpnn_internal.h"
@@ -236,9 +234,8 @@ hipError_t launch_mutual_information(hipStream_t stream, const Geometry& g, cons
                                      hipEvent_t start) {
     const int64_t per_wg = (int64_t)(kThreads / 64) * (64 / kGroup);
     const int64_t blocks = ((int64_t)g.in_hcu * g.out_hcu + per_wg - 1) / per_wg;
-    hipExtLaunchKernelGGL(mi_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, start,
-                          nullptr, 0, g, pi, pj, pij, eps, mi);
-    return hipGetLastError();
+    return launch_timed(mi_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, start,
+                        nullptr, g, pi, pj, pij, eps, mi);
 }
 
 hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const double* mi,
@@ -247,10 +244,9 @@ hipError_t launch_plasticity_swap(hipStream_t stream, const Geometry& g, const d
                                   float* w, int32_t* act_list, int32_t* act_count,
                                   int32_t* swap_count, hipEvent_t stop) {
     if (n_swaps > kMaxSwaps) return hipErrorInvalidValue;
-    hipExtLaunchKernelGGL(swap_kernel, dim3((unsigned)g.out_hcu), dim3(kThreads),
-                          (size_t)g.in_hcu, stream, nullptr, stop, 0, g, mi, n_swaps, pi, pj,
-                          pij, eps, drop_bits, mask, w, act_list, act_count, swap_count);
-    return hipGetLastError();
+    return launch_timed(swap_kernel, dim3((unsigned)g.out_hcu), dim3(kThreads),
+                        (size_t)g.in_hcu, stream, nullptr, stop, g, mi, n_swaps, pi, pj,
+                        pij, eps, drop_bits, mask, w, act_list, act_count, swap_count);
 }
 
 }  // namespace bcpnn

@@ -23,8 +23,6 @@
 //
 // MFMA f64 16x16x4 lane layout (verified on gfx950): A[i][k] from lane i + 16 k, B[k][j] from
 // lane j + 16 k, and lane l holds D[l / 16 + 4 r][l % 16] in result register r.
-#include <hip/hip_ext.h>
-
 #include <mutex>
 
 #include "bcpnn_internal.h"
@@ -518,11 +516,10 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     });
     auto go = [&](auto kernel) {
         const TraceOperands o = ops ? *ops : TraceOperands{};
-        // the events (when given) are stamped by the dispatch itself
-        hipExtLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, start,
-                              stop, 0, g, lay, x, B, w, bias, act_list, act_count, gain, mode, y,
-                              s, winner, target, o, ops ? 1 : 0);
-        return hipGetLastError();
+        // the events (when given) are recorded around the launch
+        return launch_timed(kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, start,
+                            stop, g, lay, x, B, w, bias, act_list, act_count, gain, mode, y,
+                            s, winner, target, o, ops ? 1 : 0);
     };
     if (vec == 4) {
         if (lean) return go(support_kernel<1, 4, kLeanSlots>);

@@ -58,8 +58,6 @@
 // MFMA 32x32x16 bf16 lane layout (verified on gfx950): A[i][k] for k = 8 (l / 32) + 0..7 from
 // lane l = i + 32 (k / 8), B[k][j] likewise with j = l % 32, and lane l holds
 // D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] in result register r.
-#include <hip/hip_ext.h>
-
 #include "bcpnn_internal.h"
 #include "device_common.h"
 
@@ -250,6 +248,8 @@ trace_sweep_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int stripe) {
                     op[c][2] = *reinterpret_cast<const u32x4*>(bt.t_hi + fb + ks);
                     op[c][3] = *reinterpret_cast<const u32x4*>(bt.t_lo + fb + ks);
                 }
+                // every load of the chunk issued before the first product waits on one
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int c = 0; c < kChunk; ++c) {
                     if (k0 + c < nk) {
@@ -720,6 +720,8 @@ trace_sweep_pair_kernel(Geometry g, SweepArgs a, int n_cg, int n_work, int strip
                     op[c][2] = *reinterpret_cast<const u32x4*>(bt.t_hi + fb + ks);
                     op[c][3] = *reinterpret_cast<const u32x4*>(bt.t_lo + fb + ks);
                 }
+                // every load of the chunk issued before the first product waits on one
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int c = 0; c < kPairChunk; ++c) {
                     if (k0 + c < nk) {
@@ -1359,9 +1361,8 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
         }
         const int64_t n_ti = (n_rb + tw - 1) / tw;
         const int64_t n_tj = (n_cb + cbs - 1) / cbs;
-        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(tw * 64), 0, stream,
-                              start, stop, 0, g, a, (int)n_tj);
-        return hipGetLastError();
+        return launch_timed(kernel, dim3((unsigned)(n_ti * n_tj)), dim3(tw * 64), 0, stream,
+                            start, stop, g, a, (int)n_tj);
     }
     if (resident_wgs < 0) {
         // large layer: 128 x 128 tiles, operands staged through LDS
@@ -1373,9 +1374,8 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
             default: return hipErrorInvalidValue;
         }
         const int64_t n_ti = (n_rb + 3) / 4;
-        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(n_ti * n_cg)), dim3(kWaves * 64), 0, stream,
-                              start, stop, 0, g, a, (int)n_cg);
-        return hipGetLastError();
+        return launch_timed(kernel, dim3((unsigned)(n_ti * n_cg)), dim3(kWaves * 64), 0, stream,
+                            start, stop, g, a, (int)n_cg);
     }
     void (*kernel)(Geometry, SweepArgs, int, int, int) = nullptr;
     switch (a.drop_bits * 2 + (a.paired ? 1 : 0)) {
@@ -1398,10 +1398,9 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
     int64_t stripe = (n_cg + 7) / 8;
     if (stripe * cg_bytes > kStripeBytes) stripe = kStripeBytes / cg_bytes;
     if (stripe < 1) stripe = 1;
-    // the events (when given) are stamped by the dispatch itself, so they time the kernel alone
-    hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kWaves * 64), 0, stream, start,
-                          stop, 0, g, a, (int)n_cg, (int)n_work, (int)stripe);
-    return hipGetLastError();
+    // the events (when given) are recorded around the launch
+    return launch_timed(kernel, dim3((unsigned)grid), dim3(kWaves * 64), 0, stream, start,
+                        stop, g, a, (int)n_cg, (int)n_work, (int)stripe);
 }
 
 // Row tiles of a hidden HCU's active rows (32 units, or with complement pairs 32 input HCUs)
@@ -1442,9 +1441,8 @@ hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const Trac
         case 66: kernel = trace_active_pair_kernel<16, true>; break;
         default: return hipErrorInvalidValue;
     }
-    hipExtLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kWaves * 64), 0, stream, start,
-                          stop, 0, g, a, act_list, act_count, (int)n_rt, (int)n_cgr, (int)n_work);
-    return hipGetLastError();
+    return launch_timed(kernel, dim3((unsigned)blocks), dim3(kWaves * 64), 0, stream, start,
+                        stop, g, a, act_list, act_count, (int)n_rt, (int)n_cgr, (int)n_work);
 }
 
 }  // namespace bcpnn

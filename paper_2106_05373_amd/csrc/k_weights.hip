@@ -9,8 +9,6 @@
 // the mask is set: a silent weight is 0 whatever its trace.  When N_out is a multiple of 4
 // (16-byte rows) each lane moves 16 bytes per access, eight accesses in flight, finds a column's
 // hidden HCU by a multiply-high instead of a division, and stores w with the non-temporal hint.
-#include <hip/hip_ext.h>
-
 #include "bcpnn_internal.h"
 #include "device_common.h"
 
@@ -167,6 +165,7 @@ hipError_t launch_recompute_weights(hipStream_t stream, const Geometry& g, const
                                     float* b, hipEvent_t start, hipEvent_t stop) {
     // 16-byte rows and an exact multiply-high HCU lookup (out_mcu >= 2, so that the multiplier
     // fits 32 bits): the vector kernel; else the scalar one
+    hipError_t e;
     if (g.n_out % 4 == 0 && g.out_mcu >= 2 &&
         (uint64_t)g.n_out * (uint64_t)g.out_mcu < (1ull << 32)) {
         const uint32_t magic =
@@ -174,15 +173,14 @@ hipError_t launch_recompute_weights(hipStream_t stream, const Geometry& g, const
         // one row per workgroup: short-lived workgroups keep the stores streaming (a
         // grid-stride loop over rows with fewer workgroups writes at about 5.5 against 6.3 TB/s)
         const int64_t rows = g.n_in < (int64_t)1 << 30 ? g.n_in : (int64_t)1 << 30;
-        hipExtLaunchKernelGGL(recompute_weights_vec_kernel, dim3((unsigned)rows),
-                              dim3(kSweepThreads), 0, stream, start, stop, 0, g, mask, pi, pj,
-                              pij, eps, drop_bits, magic, w);
+        e = launch_timed(recompute_weights_vec_kernel, dim3((unsigned)rows),
+                         dim3(kSweepThreads), 0, stream, start, stop, g, mask, pi, pj,
+                         pij, eps, drop_bits, magic, w);
     } else {
-        hipExtLaunchKernelGGL(recompute_weights_kernel, dim3(sweep_blocks(g)),
-                              dim3(kSweepThreads), 0, stream, start, stop, 0, g, mask, pi, pj,
-                              pij, eps, drop_bits, w);
+        e = launch_timed(recompute_weights_kernel, dim3(sweep_blocks(g)),
+                         dim3(kSweepThreads), 0, stream, start, stop, g, mask, pi, pj,
+                         pij, eps, drop_bits, w);
     }
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_bias(stream, g, pj, eps, bias_gain, b);
 }

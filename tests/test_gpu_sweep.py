@@ -330,8 +330,8 @@ def test_inputs_that_are_not_pairs_fail_loudly(pairs):
 
 def test_profile_records_each_kernel():
     """Dispatch-stamped timing of each train_batch kernel: with period 1, nine batches give nine
-    support and nine active-block launches and two sweeps (eight batches, then the one the read
-    applies); an unknown kernel is rejected."""
+    support and nine active-block launches and one sweep (of the first eight; reading leaves the
+    ninth batch queued), the flush a second sweep; an unknown kernel is rejected."""
     import torch
     xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:9]]
     lay = bcpnn().Layer(workload_config(MNIST), workload_mask(MNIST))
@@ -341,9 +341,11 @@ def test_profile_records_each_kernel():
     ms_sw, n_sw = lay.profile_read_kernel("sweep")
     ms_su, n_su = lay.profile_read_kernel("support")
     ms_ac, n_ac = lay.profile_read_kernel("active")
-    assert (n_sw, n_su, n_ac) == (2, 9, 9)
+    assert (n_sw, n_su, n_ac) == (1, 9, 9)
     assert ms_sw > 0 and ms_su > 0 and ms_ac > 0
     assert lay.profile_read_kernel("support") == (0.0, 0)          # reading clears
+    lay.flush()
+    assert lay.profile_read_kernel("sweep")[1] == 1                 # the ninth batch's sweep
     B = bcpnn()
     import ctypes
     ms, n = ctypes.c_double(), ctypes.c_int32()
