@@ -339,6 +339,15 @@ __device__ __forceinline__ void stage_barrier() {
 // s_waitcnt immediate with vmcnt = n (6 bits) and the other counters left alone.
 constexpr int vm_wait(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
+// Stage buffer index as a type.  The two stage buffers of a tiled sweep are separate LDS arrays
+// and the chunk loop is unrolled by two, so that every access names its buffer at compile time:
+// the compiler then knows that a chunk's LDS reads do not touch the buffer that the next
+// chunk's direct-to-LDS loads are filling, and lets those loads run under the chunk's products.
+// (With one array indexed by the chunk's parity it cannot tell the buffers apart and waits for
+// the next chunk's loads before the first read of the current one.)
+template <int V>
+struct StageIx { static constexpr int value = V; };
+
 constexpr int kTileKC = 2;
 constexpr int kPairTileCB = 3;   // column blocks per workgroup of the tiled sweep with pairs
 constexpr int kSumTileCB = 8;    // column blocks per workgroup of the sum-form sweep
@@ -349,7 +358,8 @@ __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_e
 trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     constexpr int kItems = 8 * kKC;                 // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kWaves;
-    __shared__ u32x4 stage[2][kItems][64];
+    __shared__ u32x4 stage0[kItems][64];
+    __shared__ u32x4 stage1[kItems][64];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
@@ -396,7 +406,8 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     // (item = (k-step in chunk * 4 + column block) * 2 + {hi, lo}, wave w issuing w, w + 4, ...)
     // and this wave's x fragments into xn
     u32x4 xc[kKC][2], xn[kKC][2];
-    auto request = [&](int t, int k0, int sb) {
+    auto request = [&](int t, int k0, auto sb_c) {
+        u32x4 (*const st)[64] = decltype(sb_c)::value == 0 ? stage0 : stage1;
         const SweepBatch bt = a.bt[t];
 #pragma unroll
         for (int q = 0; q < kPerWave; ++q) {
@@ -408,7 +419,7 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
             const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
                                   (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
             __builtin_amdgcn_global_load_lds((const void*)src,
-                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+                (void __attribute__((address_space(3)))*)&st[item][0], 16, 0, 0);
         }
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
@@ -424,14 +435,17 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     };
 
     int dt = 0, dk = 0;
-    request(dt, dk, 0);
+    request(dt, dk, StageIx<0>{});
     next(dt, dk);
 
     f16v acc[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] = f16v{};
     int ct = 0, ck = 0;
-    for (int lc = 0; lc < n_ch; ++lc) {
+    // chunk lc, its t items in stage buffer sb_c (lc's parity)
+    auto chunk = [&](int lc, auto sb_c) {
+        constexpr int sb = decltype(sb_c)::value;
+        const u32x4 (*const st)[64] = sb == 0 ? stage0 : stage1;
         // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
         // items visible to every wave and tells that every wave is done with the other buffer
         __builtin_amdgcn_s_waitcnt(vm_wait(0));
@@ -442,10 +456,9 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
         }
         stage_barrier();
         if (lc + 1 < n_ch) {
-            request(dt, dk, (lc + 1) & 1);
+            request(dt, dk, StageIx<1 - sb>{});
             next(dt, dk);
         }
-        const int sb = lc & 1;
         const int nk = a.bt[ct].nk;
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
@@ -455,8 +468,8 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
                 bf8 bh[4], bl[4];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 4 + c) * 2][lane]);
-                    bl[c] = __builtin_bit_cast(bf8, stage[sb][(kq * 4 + c) * 2 + 1][lane]);
+                    bh[c] = __builtin_bit_cast(bf8, st[(kq * 4 + c) * 2][lane]);
+                    bl[c] = __builtin_bit_cast(bf8, st[(kq * 4 + c) * 2 + 1][lane]);
                 }
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
@@ -480,6 +493,10 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
             }
         }
         next(ct, ck);
+    };
+    for (int lc = 0; lc < n_ch; lc += 2) {
+        chunk(lc, StageIx<0>{});
+        if (lc + 1 < n_ch) chunk(lc + 1, StageIx<1>{});
     }
     if (!live) return;
 #pragma unroll
@@ -768,7 +785,8 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kWaves;
     static_assert(kPerWave * kWaves == kItems, "t items split evenly over the waves");
-    __shared__ u32x4 stage[2][kItems][64];
+    __shared__ u32x4 stage0[kItems][64];
+    __shared__ u32x4 stage1[kItems][64];
     __shared__ float stot[kMaxSweepBatches][32 * kCB];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -823,7 +841,8 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     // (item = (k-step in chunk * kCB + column block) * 2 + {hi, lo}, wave w issuing w, w + 4,
     // ...) and this wave's x fragments into xn
     u32x4 xc[kKC][2], xn[kKC][2];
-    auto request = [&](int t, int k0, int sb) {
+    auto request = [&](int t, int k0, auto sb_c) {
+        u32x4 (*const st)[64] = decltype(sb_c)::value == 0 ? stage0 : stage1;
         const SweepBatch bt = a.bt[t];
 #pragma unroll
         for (int q = 0; q < kPerWave; ++q) {
@@ -835,7 +854,7 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
             const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
                                   (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
             __builtin_amdgcn_global_load_lds((const void*)src,
-                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+                (void __attribute__((address_space(3)))*)&st[item][0], 16, 0, 0);
         }
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
@@ -851,7 +870,7 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
     };
 
     int dt = 0, dk = 0;
-    request(dt, dk, 0);
+    request(dt, dk, StageIx<0>{});
     next(dt, dk);
 
     // column totals of every queued batch for the workgroup's 32 kCB columns (clamped)
@@ -871,7 +890,10 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
 #pragma unroll
     for (int c = 0; c < kCB; ++c) acc[c] = f16v{};
     int ct = 0, ck = 0;
-    for (int lc = 0; lc < n_ch; ++lc) {
+    // chunk lc, its t items in stage buffer sb_c (lc's parity)
+    auto chunk = [&](int lc, auto sb_c) {
+        constexpr int sb = decltype(sb_c)::value;
+        const u32x4 (*const st)[64] = sb == 0 ? stage0 : stage1;
         // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
         // items visible to every wave and tells that every wave is done with the other buffer
         __builtin_amdgcn_s_waitcnt(vm_wait(0));
@@ -882,10 +904,9 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
         }
         stage_barrier();
         if (lc + 1 < n_ch) {
-            request(dt, dk, (lc + 1) & 1);
+            request(dt, dk, StageIx<1 - sb>{});
             next(dt, dk);
         }
-        const int sb = lc & 1;
         const int nk = a.bt[ct].nk;
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
@@ -896,13 +917,13 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
                 bf8 bh[kCB];
 #pragma unroll
                 for (int c = 0; c < kCB; ++c)
-                    bh[c] = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2][lane]);
+                    bh[c] = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2][lane]);
 #pragma unroll
                 for (int c = 0; c < kCB; ++c)
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh[c], acc[c], 0, 0, 0);
 #pragma unroll
                 for (int c = 0; c < kCB; ++c) {
-                    const bf8 bl = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
+                    const bf8 bl = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2 + 1][lane]);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[c], 0, 0, 0);
                 }
 #pragma unroll
@@ -925,6 +946,10 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
             }
         }
         next(ct, ck);
+    };
+    for (int lc = 0; lc < n_ch; lc += 2) {
+        chunk(lc, StageIx<0>{});
+        if (lc + 1 < n_ch) chunk(lc + 1, StageIx<1>{});
     }
     if (!live) return;
 #pragma unroll
@@ -957,7 +982,8 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
 // trip to memory feeds 8 / 3 times the matrix-core work.  kTW waves share the t items.
 // Measured on the STL-shaped layer (6.67 batches per launch, each variant beside the previous
 // one on one box): 4.16 ms per launch per-batch (trace_sweep_pair_tile_kernel), 3.49 ms with
-// kCB = 6, 3.33 ms with kCB = 8; 8 waves of kCB = 6 (256 input HCUs) 3.84 ms.  The result differs from per-batch updates by the
+// kCB = 6, 3.33 ms with kCB = 8; 8 waves of kCB = 6 (256 input HCUs) 3.84 ms; 3.05 ms with the
+// stage buffers as two arrays (StageIx), so that the next chunk's loads run under the products.  The result differs from per-batch updates by the
 // fp32 rounding of the regrouped sums (a few ulps per batch), not by more.
 template <int kKC, int kCB, int kTW>
 __global__ void __launch_bounds__(kTW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -965,7 +991,8 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
     constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kTW;
     static_assert(kPerWave * kTW == kItems, "t items split evenly over the waves");
-    __shared__ u32x4 stage[2][kItems][64];
+    __shared__ u32x4 stage0[kItems][64];
+    __shared__ u32x4 stage1[kItems][64];
     __shared__ float stot[32 * kCB];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -994,7 +1021,8 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
     for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
     // requests of the chunk at (batch t, first k-step k0), as in trace_sweep_pair_tile_kernel
     u32x4 xc[kKC][2], xn[kKC][2];
-    auto request = [&](int t, int k0, int sb) {
+    auto request = [&](int t, int k0, auto sb_c) {
+        u32x4 (*const st)[64] = decltype(sb_c)::value == 0 ? stage0 : stage1;
         const SweepBatch bt = a.bt[t];
 #pragma unroll
         for (int q = 0; q < kPerWave; ++q) {
@@ -1006,7 +1034,7 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
             const uint16_t* src = (half ? bt.t_lo : bt.t_hi) +
                                   (((int64_t)blk * n_ks + ks) * 64 + lane) * 8;
             __builtin_amdgcn_global_load_lds((const void*)src,
-                (void __attribute__((address_space(3)))*)&stage[sb][item][0], 16, 0, 0);
+                (void __attribute__((address_space(3)))*)&st[item][0], 16, 0, 0);
         }
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
@@ -1022,7 +1050,7 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
     };
 
     int dt = 0, dk = 0;
-    request(dt, dk, 0);
+    request(dt, dk, StageIx<0>{});
     next(dt, dk);
 
     // Stot of the workgroup's 32 kCB columns (clamped), batch by batch in order
@@ -1044,7 +1072,10 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
 #pragma unroll
     for (int c = 0; c < kCB; ++c) acc[c] = f16v{};
     int ct = 0, ck = 0;
-    for (int lc = 0; lc < n_ch; ++lc) {
+    // chunk lc, its t items in stage buffer sb_c (lc's parity)
+    auto chunk = [&](int lc, auto sb_c) {
+        constexpr int sb = decltype(sb_c)::value;
+        const u32x4 (*const st)[64] = sb == 0 ? stage0 : stage1;
         // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
         // items visible to every wave and tells that every wave is done with the other buffer
         __builtin_amdgcn_s_waitcnt(vm_wait(0));
@@ -1055,10 +1086,9 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
         }
         stage_barrier();
         if (lc + 1 < n_ch) {
-            request(dt, dk, (lc + 1) & 1);
+            request(dt, dk, StageIx<1 - sb>{});
             next(dt, dk);
         }
-        const int sb = lc & 1;
         if (ck == 0 && ct > 0) {
             // batch ct starts: acc holds R_{ct-1} / c2_{ct-1}; make it R_{ct-1} c1_ct / c2_ct
             const float sc = a.bt[ct].c1 * (a.bt[ct - 1].c2 / a.bt[ct].c2);
@@ -1075,8 +1105,8 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
                 const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
 #pragma unroll
                 for (int c = 0; c < kCB; ++c) {
-                    const bf8 bh = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2][lane]);
-                    const bf8 bl = __builtin_bit_cast(bf8, stage[sb][(kq * kCB + c) * 2 + 1][lane]);
+                    const bf8 bh = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2][lane]);
+                    const bf8 bl = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2 + 1][lane]);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[c], 0, 0, 0);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[c], 0, 0, 0);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[c], 0, 0, 0);
@@ -1084,6 +1114,10 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
             }
         }
         next(ct, ck);
+    };
+    for (int lc = 0; lc < n_ch; lc += 2) {
+        chunk(lc, StageIx<0>{});
+        if (lc + 1 < n_ch) chunk(lc + 1, StageIx<1>{});
     }
     stage_barrier();                                    // stot is visible to every wave
 
