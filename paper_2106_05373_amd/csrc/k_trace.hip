@@ -352,6 +352,8 @@ constexpr int kTileKC = 2;
 constexpr int kPairTileCB = 3;   // column blocks per workgroup of the tiled sweep with pairs
 constexpr int kSumTileCB = 8;    // column blocks per workgroup of the sum-form sweep
 constexpr int kSumTileWaves = 4; // waves (blocks of 32 input HCUs) per workgroup of it
+constexpr int kSumTileKC = 1;    // k-steps per chunk of it
+constexpr int kSumTileStages = 4;   // its stage buffers: chunks in flight + 1
 
 template <int kDropBits, int kKC>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -978,22 +980,38 @@ trace_sweep_pair_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
 // accumulate R / c2_t in place (the accumulator is scaled by c1_t c2_{t-1} / c2_t before batch
 // t's products), so the old traces are read only in the epilogue, and the registers they take
 // in trace_sweep_pair_tile_kernel hold more accumulators instead: a wave covers 32 kCB columns
-// (kCB = 8 against 3) with the same operand pipeline (one chunk in flight), so that each round
-// trip to memory feeds 8 / 3 times the matrix-core work.  kTW waves share the t items.
+// (kCB = 8 against 3), so that each operand byte feeds 8 / 3 times the matrix-core work.  kTW
+// waves share the t items, which stream through kStages LDS buffers of kKC k-steps (kStages - 1
+// chunks in flight; a wave's x fragments likewise through kStages register sets); column block
+// c + 1's t fragments are read from LDS during block c's products.
 // Measured on the STL-shaped layer (6.67 batches per launch, each variant beside the previous
 // one on one box): 4.16 ms per launch per-batch (trace_sweep_pair_tile_kernel), 3.49 ms with
 // kCB = 6, 3.33 ms with kCB = 8; 8 waves of kCB = 6 (256 input HCUs) 3.84 ms; 3.05 ms with the
-// stage buffers as two arrays (StageIx), so that the next chunk's loads run under the products.  The result differs from per-batch updates by the
+// stage buffers as separate arrays (StageIx), so that the next chunk's loads run under the
+// products; four stages of one k-step instead of two of two 2.99 ms; the LDS reads one block
+// ahead 2.94 ms; the column totals' loads issued all at once 2.75-2.80 ms.  Per workgroup (time
+// stamps, 7 batches, the kernel alone): prologue 7 us, products 107 us, epilogue 26 us.  The result differs from per-batch updates by the
 // fp32 rounding of the regrouped sums (a few ulps per batch), not by more.
-template <int kKC, int kCB, int kTW>
+template <int kKC, int kCB, int kTW, int kStages>
 __global__ void __launch_bounds__(kTW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
     constexpr int kItems = 2 * kCB * kKC;           // 1 KiB t items per chunk
     constexpr int kPerWave = kItems / kTW;
     static_assert(kPerWave * kTW == kItems, "t items split evenly over the waves");
+    static_assert(kStages >= 2 && kStages <= 4, "two to four stage buffers");
+    // memory loads a wave issues per chunk: its share of the t items and its x fragments
+    constexpr int kLoads = kPerWave + 2 * kKC;
     __shared__ u32x4 stage0[kItems][64];
     __shared__ u32x4 stage1[kItems][64];
-    __shared__ float stot[32 * kCB];
+    __shared__ u32x4 stage2[kStages > 2 ? kItems : 1][64];
+    __shared__ u32x4 stage3[kStages > 3 ? kItems : 1][64];
+    auto buf = [&](auto sb_c) -> u32x4 (*)[64] {
+        constexpr int b = decltype(sb_c)::value;
+        if constexpr (b == 0) return stage0;
+        else if constexpr (b == 1) return stage1;
+        else if constexpr (b == 2) return stage2;
+        else return stage3;
+    };    __shared__ float stot[32 * kCB];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n_out = (int)g.n_out;
@@ -1019,10 +1037,12 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
 
     int n_ch = 0;
     for (int t = 0; t < a.n_batches; ++t) n_ch += (a.bt[t].nk + kKC - 1) / kKC;
-    // requests of the chunk at (batch t, first k-step k0), as in trace_sweep_pair_tile_kernel
-    u32x4 xc[kKC][2], xn[kKC][2];
+    // requests of the chunk at (batch t, first k-step k0) into stage sb_c: its t items into
+    // that stage buffer, the wave's x fragments into xs[sb_c]
+    u32x4 xs[kStages][kKC][2];
     auto request = [&](int t, int k0, auto sb_c) {
-        u32x4 (*const st)[64] = decltype(sb_c)::value == 0 ? stage0 : stage1;
+        constexpr int sb = decltype(sb_c)::value;
+        u32x4 (*const st)[64] = buf(sb_c);
         const SweepBatch bt = a.bt[t];
 #pragma unroll
         for (int q = 0; q < kPerWave; ++q) {
@@ -1040,30 +1060,60 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
         for (int kq = 0; kq < kKC; ++kq) {
             const int ks = k0 + kq < bt.nk ? k0 + kq : bt.nk - 1;
             const int64_t fa = (((int64_t)bic * n_ks + ks) * 64 + lane) * 8;
-            xn[kq][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa);
-            xn[kq][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa);
+            xs[sb][kq][0] = *reinterpret_cast<const u32x4*>(bt.x_hi + fa);
+            xs[sb][kq][1] = *reinterpret_cast<const u32x4*>(bt.x_lo + fa);
         }
     };
     auto next = [&](int& t, int& k0) {
         k0 += kKC;
         if (k0 >= a.bt[t].nk) { k0 = 0; ++t; }
     };
+    // the chunk after (t, k0) for the requests, which stay on the last chunk past the end: every
+    // chunk requests the one kStages - 1 ahead, unconditionally, so that a wave always has the
+    // same number of loads in flight (past the end, reloads of the last chunk that nothing reads)
+    auto next_req = [&](int& t, int& k0) {
+        k0 += kKC;
+        if (k0 >= a.bt[t].nk) {
+            if (t + 1 < a.n_batches) { k0 = 0; ++t; }
+            else k0 -= kKC;
+        }
+    };
 
+    // the first kStages - 1 chunks
     int dt = 0, dk = 0;
     request(dt, dk, StageIx<0>{});
-    next(dt, dk);
+    next_req(dt, dk);
+    if constexpr (kStages > 2) { request(dt, dk, StageIx<1>{}); next_req(dt, dk); }
+    if constexpr (kStages > 3) { request(dt, dk, StageIx<2>{}); next_req(dt, dk); }
 
-    // Stot of the workgroup's 32 kCB columns (clamped), batch by batch in order
-    for (int cl = threadIdx.x; cl < 32 * kCB; cl += kTW * 64) {
+    // Stot of the workgroup's 32 kCB columns (clamped; one per thread): the column-sum tiles
+    // of every queued batch requested at once (batch and tile clamped), then added in tile
+    // order (as marginal_colsum) and combined batch by batch in order
+    static_assert(32 * kCB == kTW * 64, "one Stot column per thread");
+    {
+        constexpr int kParts = 16;                      // tiles requested up front per batch
+        const int cl = threadIdx.x;
         const int col = j00 + cl < n_out ? j00 + cl : n_out - 1;
-        float v = 0.0f;
-        for (int t = 0; t < a.n_batches; ++t) {
-            const SweepBatch bt = a.bt[t];
-            MarginalIn m;
+        float part[kMaxSweepBatches][kParts];
 #pragma unroll
-            for (int q = 0; q < kSums; ++q)
-                m.part[q] = bt.t_sum[(int64_t)(q < bt.nk ? q : bt.nk - 1) * n_out + col];
-            v = fmaf(bt.c2, marginal_colsum(m, bt.t_sum, n_out, col, bt.nk), v * bt.c1);
+        for (int t = 0; t < kMaxSweepBatches; ++t) {
+            const SweepBatch& bt = a.bt[t < a.n_batches ? t : a.n_batches - 1];
+#pragma unroll
+            for (int q = 0; q < kParts; ++q)
+                part[t][q] = bt.t_sum[(int64_t)(q < bt.nk ? q : bt.nk - 1) * n_out + col];
+        }
+        float v = 0.0f;
+#pragma unroll
+        for (int t = 0; t < kMaxSweepBatches; ++t) {
+            if (t < a.n_batches) {
+                const SweepBatch& bt = a.bt[t];
+                float colsum = 0.0f;
+#pragma unroll
+                for (int q = 0; q < kParts; ++q)
+                    if (q < bt.nk) colsum += part[t][q];
+                for (int q = kParts; q < bt.nk; ++q) colsum += bt.t_sum[(int64_t)q * n_out + col];
+                v = fmaf(bt.c2, colsum, v * bt.c1);
+            }
         }
         stot[cl] = v;
     }
@@ -1072,23 +1122,18 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
 #pragma unroll
     for (int c = 0; c < kCB; ++c) acc[c] = f16v{};
     int ct = 0, ck = 0;
-    // chunk lc, its t items in stage buffer sb_c (lc's parity)
-    auto chunk = [&](int lc, auto sb_c) {
+    // chunk lc, in stage sb_c = lc mod kStages
+    auto chunk = [&](int lc, auto sb_c) __attribute__((always_inline)) {
         constexpr int sb = decltype(sb_c)::value;
-        const u32x4 (*const st)[64] = sb == 0 ? stage0 : stage1;
-        // chunk lc's requests were the last issued: wait for all, then the barrier makes its t
-        // items visible to every wave and tells that every wave is done with the other buffer
-        __builtin_amdgcn_s_waitcnt(vm_wait(0));
-#pragma unroll
-        for (int kq = 0; kq < kKC; ++kq) {
-            xc[kq][0] = xn[kq][0];
-            xc[kq][1] = xn[kq][1];
-        }
+        const u32x4 (*const st)[64] = buf(sb_c);
+        // wait for this wave's loads of chunk lc (those of the kStages - 2 chunks issued after
+        // it stay in flight), then the barrier makes every wave's t items of it visible and
+        // tells that every wave is done with chunk lc - 1, whose buffer the request refills
+        __builtin_amdgcn_s_waitcnt(vm_wait((kStages - 2) * kLoads));
         stage_barrier();
-        if (lc + 1 < n_ch) {
-            request(dt, dk, StageIx<1 - sb>{});
-            next(dt, dk);
-        }
+        request(dt, dk, StageIx<(sb + kStages - 1) % kStages>{});
+        next_req(dt, dk);
+        const auto& xc = xs[sb];
         if (ck == 0 && ct > 0) {
             // batch ct starts: acc holds R_{ct-1} / c2_{ct-1}; make it R_{ct-1} c1_ct / c2_ct
             const float sc = a.bt[ct].c1 * (a.bt[ct - 1].c2 / a.bt[ct].c2);
@@ -1100,25 +1145,59 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
         const int nk = a.bt[ct].nk;
 #pragma unroll
         for (int kq = 0; kq < kKC; ++kq) {
-            if (ck + kq < nk) {
+            // (a chunk of one k-step is never past its batch: no branch around the products,
+            // which would hide from the compiler that their x loads were waited for)
+            if (kKC == 1 || ck + kq < nk) {
                 const bf8 ah = __builtin_bit_cast(bf8, xc[kq][0]);
                 const bf8 al = __builtin_bit_cast(bf8, xc[kq][1]);
+                // column block c + 1's t fragments are read from LDS before block c's products,
+                // so that their latency passes under them
+                bf8 bh = __builtin_bit_cast(bf8, st[(kq * kCB) * 2][lane]);
+                bf8 bl = __builtin_bit_cast(bf8, st[(kq * kCB) * 2 + 1][lane]);
 #pragma unroll
                 for (int c = 0; c < kCB; ++c) {
-                    const bf8 bh = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2][lane]);
-                    const bf8 bl = __builtin_bit_cast(bf8, st[(kq * kCB + c) * 2 + 1][lane]);
+                    bf8 bhn = bh, bln = bl;
+                    if (c + 1 < kCB) {
+                        bhn = __builtin_bit_cast(bf8, st[(kq * kCB + c + 1) * 2][lane]);
+                        bln = __builtin_bit_cast(bf8, st[(kq * kCB + c + 1) * 2 + 1][lane]);
+                    }
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[c], 0, 0, 0);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[c], 0, 0, 0);
                     acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[c], 0, 0, 0);
+                    bh = bhn;
+                    bl = bln;
+                }
+#pragma unroll
+                for (int c = 0; c < kCB; ++c) {
+                    if (c == 0) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // LDS reads
+                    if (c + 1 < kCB) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 3, 0);               // MFMA
                 }
             }
         }
         next(ct, ck);
     };
-    for (int lc = 0; lc < n_ch; lc += 2) {
+    // kStages chunks from lc; whether chunks remain after them
+    auto group = [&](int lc) __attribute__((always_inline)) -> bool {
         chunk(lc, StageIx<0>{});
-        if (lc + 1 < n_ch) chunk(lc + 1, StageIx<1>{});
-    }
+        if (lc + 1 >= n_ch) return false;
+        chunk(lc + 1, StageIx<1>{});
+        if constexpr (kStages > 2) {
+            if (lc + 2 >= n_ch) return false;
+            chunk(lc + 2, StageIx<2>{});
+        }
+        if constexpr (kStages > 3) {
+            if (lc + 3 >= n_ch) return false;
+            chunk(lc + 3, StageIx<3>{});
+        }
+        return lc + kStages < n_ch;
+    };
+    // (the first group outside the loop: the loop is then entered with the loads in flight
+    // that its back edge carries, and the compiler's count of them stays exact)
+    bool more = group(0);
+    for (int lc = kStages; more; lc += kStages) more = group(lc);
+    // (the reloads past the end land in LDS before the workgroup may end)
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
     stage_barrier();                                    // stot is visible to every wave
 
     // ---- epilogue: P_n = c1^n P_0 + R, P2_n = c1^n P2_0 + Stot - R, silent elements; column
@@ -1135,8 +1214,10 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
     float c1n = 1.0f;
     for (int t = 0; t < a.n_batches; ++t) c1n *= a.bt[t].c1;
     const float c2n = a.bt[a.n_batches - 1].c2;
-    // old traces of column block c, both rows of each pair (requested one pass ahead)
-    float pold[2][2][16];
+    // old traces of column block c, both rows of each pair (requested kEpiDepth - 1 blocks
+    // ahead, into slot c mod kEpiDepth)
+    constexpr int kEpiDepth = 2;
+    float pold[kEpiDepth][2][16];
     auto request_old = [&](int c, int slot) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -1157,30 +1238,32 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
                                  : (jc + (lane - 32 < cols ? lane - 32 : cols - 1)) / g.out_mcu;
         act_bits[c] = block_mask_bits_hu(g, a.mask, hu, lane);
     }
-    request_old(0, 0);
+#pragma unroll
+    for (int c = 0; c + 1 < kEpiDepth; ++c) request_old(c, c);
 #pragma unroll
     for (int c = 0; c < kCB; ++c) {
-        if (c + 1 < kCB) request_old(c + 1, (c + 1) & 1);
+        if (c + kEpiDepth - 1 < kCB) request_old(c + kEpiDepth - 1, (c + kEpiDepth - 1) % kEpiDepth);
         const int j0 = j00 + 32 * c;
         if (live) {                                             // wave-uniform
             const bool jok = j0 + jl < n_out;
             const float st = stot[32 * c + jl];
+            const uint32_t act = act_bits[c];
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int il = il0 + 8 * (r >> 2) + (r & 3);
                 const float R = c2n * acc[c][r];
-                const float pe = fmaf(c1n, pold[c & 1][0][r], R);
-                const float po = fmaf(c1n, pold[c & 1][1][r], st - R);
+                const float pe = fmaf(c1n, pold[c % kEpiDepth][0][r], R);
+                const float po = fmaf(c1n, pold[c % kEpiDepth][1][r], st - R);
                 const uint32_t off = rowoff[r] + 128u * c;
-                const bool keep = jok && !((act_bits[c] >> il) & 1u);
+                const bool keep = jok && !((act >> il) & 1u);
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(pe), rp, keep ? off : kDrop,
                                                       0, 0);
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(po), rp,
                                                       keep ? off + odd : kDrop, 0, 0);
             }
         }
-        // (a compiler fence: block c + 2's loads, into this block's registers, stay after
-        // this block's stores)
+        // (a compiler fence: block c + kEpiDepth's loads, into this block's registers, stay
+        // after this block's stores)
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
     }
 }
@@ -1385,7 +1468,8 @@ hipError_t launch_trace_sweep(hipStream_t stream, const Geometry& g, const Sweep
         int cbs = kPairTileCB, tw = kWaves;
         switch (a.drop_bits) {
             case 0:
-                kernel = trace_sweep_pair_tile_sum_kernel<kTileKC, kSumTileCB, kSumTileWaves>;
+                kernel = trace_sweep_pair_tile_sum_kernel<kSumTileKC, kSumTileCB, kSumTileWaves,
+                                                          kSumTileStages>;
                 cbs = kSumTileCB;
                 tw = kSumTileWaves;
                 break;
