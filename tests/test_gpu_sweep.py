@@ -232,6 +232,37 @@ def test_tiled_sweep_on_a_ragged_large_layer(pairs, storage):
     pair.close()
 
 
+@pytest.mark.parametrize("storage", ["f32", "bf16"])
+def test_tiled_sweep_with_batches_past_sixteen_k_steps(storage):
+    """The tiled sweeps of a large paired layer with batches of up to 300 rows (19 k-steps: the
+    column totals past the first sixteen tiles taken one by one, chunks past sixteen k-steps),
+    mixed with small ones, against the oracle as in the ragged test above."""
+    from pairs import gpu_config
+    in_hcu, out_hcu, out_mcu = 4100, 21, 100
+    rng = np.random.default_rng(13)
+    mask = np.stack([synth.random_mask(in_hcu, 1, 104, 110 + c)[:, 0] for c in range(out_hcu)], 1)
+    pair = Pair(gpu_config(in_hcu, 2, out_hcu, out_mcu, 300, alpha=0.05, complement_pairs=1,
+                           storage=storage), mask)
+    prior = pair.ora.get_state()
+    moved = Moved(pair.ora, decay(pair.cfg))
+    sizes = (300, 17, 272, 300)
+    for B in sizes:
+        p = rng.random((B, in_hcu)).astype(np.float32)
+        x = synth.encode_pixels(p)
+        win = rng.integers(0, out_mcu, size=(B, out_hcu))
+        target = np.zeros((B, out_hcu, out_mcu), np.float32)
+        np.put_along_axis(target, win[..., None], 1.0, axis=-1)
+        moved.before()
+        pair.train(x, target.reshape(B, -1))
+        moved.after()
+    sg, so = pair.gpu.get_state(), pair.ora.get_state()
+    if storage == "f32":
+        assert_state_close(sg, so, where="tiled sweep, batches past 16 k-steps")
+    check_run(prior, sg, so, pair.cfg, storage, "tiled sweep, batches past 16 k-steps",
+              len(sizes), moved)
+    pair.close()
+
+
 def test_large_layer_sum_form_grouping():
     """A large layer with complement pairs and fp32 storage sweeps its silent blocks in sum
     form (the queued batches' updates regrouped as c1^n P + R): the same batches run freely
