@@ -33,6 +33,11 @@ namespace {
 
 typedef double d4 __attribute__((ext_vector_type(4)));
 
+// Buffer resource over [p, p + bytes): loads past the range return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t input_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+
 constexpr int kRows = 16;          // batch rows per workgroup
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
@@ -206,14 +211,18 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     const int n_pass = (int)((c1 - c0 + 63) / 64);
     const int pass0 = kWaves - 1 - wave;
     float xcol[kRows];
+    // The rows are read through a buffer resource over the batch, so the rows past B read as
+    // zero and all 16 loads are unconditional.  (Clamped to a valid row instead, the loads of
+    // the rows past B shared one value, and the compiler loaded that row first and issued the
+    // others only after it arrived.)  The launch checks that the offsets fit in 32 bits.
+    const __amdgpu_buffer_rsrc_t xrs = input_rsrc(x, (uint32_t)((int64_t)B * g.n_in * 4));
     auto split_load = [&](int p) {
         const int64_t i = c0 + (int64_t)p * 64 + lane;
         const int64_t ic = i < c1 ? i : c1 - 1;
 #pragma unroll
-        for (int r = 0; r < kRows; ++r) {
-            const int rr = r < rows ? row0 + r : row0;
-            xcol[r] = x[(int64_t)rr * g.n_in + ic];
-        }
+        for (int r = 0; r < kRows; ++r)
+            xcol[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                xrs, (uint32_t)(((int64_t)(row0 + r) * g.n_in + ic) * 4), 0, 0));
     };
     // With complement pairs every pair (x_2p, x_2p+1) of these rows must add up to 1.  The
     // range starts at an even column and passes are 64 columns wide, so the partner of an even
@@ -495,6 +504,8 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     const bool lean = vec == 4 && lay.n_tiles <= kWaves && lay.kc < max_active * g.in_mcu;
     if (lean) lay = make_layout(g, B, max_active * g.in_mcu, vec, kLeanSlots);
     if (!lay.fits) return hipErrorInvalidValue;
+    // the input rows of the last row tile (up to 15 past B) must have 32-bit byte offsets
+    if ((int64_t)lay.n_row_tiles * kRows * g.n_in * 4 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;
     const size_t lds = lds_bytes(lay);
     const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
     const int64_t blocks = (int64_t)lay.n_row_tiles * g.out_hcu;
