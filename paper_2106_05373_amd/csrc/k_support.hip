@@ -255,6 +255,48 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             ops.x_sum[(int64_t)rt * g.n_in + i] = sum;
         }
     };
+    // With at most kWaves / 2 passes, each pass is split by two waves, rows 0-7 and 8-15 (task
+    // q = kWaves - 1 - wave: pass q / 2, half q % 2): half the pair checks, conversions and
+    // stores per wave.  The column sum is the two half sums added (as for t), exchanged through
+    // the input panel's LDS, free by then.
+    // (the panel lies past the support tile, which the t split reads meanwhile, when kc >= 16)
+    const bool halves = has_ops && n_pass <= kWaves / 2 && kc >= kRows;
+    const int hq = kWaves - 1 - wave, hpass = hq >> 1, hhalf = hq & 1;
+    const bool hlive = halves && hpass < n_pass;
+    float xh[kRows / 2];
+    auto half_load = [&]() {
+        const int64_t i = c0 + (int64_t)hpass * 64 + lane;
+        const int64_t ic = i < c1 ? i : c1 - 1;
+#pragma unroll
+        for (int r = 0; r < kRows / 2; ++r)
+            xh[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                xrs, (uint32_t)(((int64_t)(row0 + 8 * hhalf + r) * g.n_in + ic) * 4), 0, 0));
+    };
+    float* hsum = xs;                                    // [n_pass][2][64] after the products
+    auto half_store = [&]() {
+        const int64_t i = c0 + (int64_t)hpass * 64 + lane;
+        float sum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < kRows / 2; ++r) {
+            xh[r] = 8 * hhalf + r < rows ? xh[r] : 0.0f;
+            sum += xh[r];
+        }
+        if (ops.paired) {
+            const bool first = i < c1 && (i & 1) == 0;
+            bool bad = false;
+#pragma unroll
+            for (int r = 0; r < kRows / 2; ++r) {
+                const float nb = __shfl_down(xh[r], 1, 64);
+                bad |= first && 8 * hhalf + r < rows && !(fabsf(xh[r] + nb - 1.0f) <= kPairTolerance);
+            }
+            if (bad) *ops.pair_error = 1;
+        }
+        if (i < c1) {
+            if (!ops.paired) write_split_half(xh, ops.x_hi, ops.x_lo, i, rt, hhalf, ops.n_ks);
+            else if ((i & 1) == 0) write_split_half(xh, ops.x_hi, ops.x_lo, i >> 1, rt, hhalf, ops.n_ks);
+        }
+        hsum[(hpass * 2 + hhalf) * 64 + lane] = sum;
+    };
 
     if (k_total > 0) load_chunk(0);
     // Bias of this wave's columns, fetched now so that its latency hides behind the contraction
@@ -318,7 +360,8 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
     }
     lds_barrier();
 
-    if (has_ops && pass0 < n_pass) split_load(pass0);
+    if (hlive) half_load();
+    else if (has_ops && !halves && pass0 < n_pass) split_load(pass0);
 
     // Each wave takes rows wave and wave + 8 together (independent reduction chains), one LDS
     // read per element: lane l holds columns l, l + 64, ... of both rows in registers
@@ -437,9 +480,20 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             if (half == 0) ops.t_sum[(int64_t)rt * g.n_out + col] = total;
         }
     }
-    for (int p = pass0; p < n_pass; p += kWaves) {
-        if (p != pass0) split_load(p);
-        split_store(p);
+    if (halves) {
+        if (hlive) half_store();
+        lds_barrier();
+        if (hlive && hhalf == 0) {
+            const int64_t i = c0 + (int64_t)hpass * 64 + lane;
+            if (i < c1)
+                ops.x_sum[(int64_t)rt * g.n_in + i] =
+                    hsum[(hpass * 2) * 64 + lane] + hsum[(hpass * 2 + 1) * 64 + lane];
+        }
+    } else {
+        for (int p = pass0; p < n_pass; p += kWaves) {
+            if (p != pass0) split_load(p);
+            split_store(p);
+        }
     }
 }
 
