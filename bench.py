@@ -14,10 +14,14 @@ queues and applies a few batches at a time) are inside it, and no kernel in it c
 profiling events.
 
 After the timed region, an untimed profiling pass continues the same schedule with every
-kernel launch bracketed by HIP events recorded on its stream right before and after it; the
-kernel durations of the JSON line come from it: the roofline position of the
-dominant kernel (the sweep over the silent elements of Pij), the support and active-block
-kernels of the caller's stream, and the structural update.  The line also carries the
+kernel launch timed: the sweep, the weight pass and the structural update by HIP events
+recorded on their stream right before and after them, the support and active-block kernels
+(short launches on the caller's stream) by the device clock, stamped when their first
+workgroup starts and their last one ends; the kernel durations of the JSON line come from it: the roofline position of the
+dominant kernel (the one with the most GPU time per batch: the support, the active-block
+trace kernel, or the sweep over the silent elements of Pij, per batch of its launch), the
+sweep against the HBM roofline and the support against the fp64 matrix cores whichever
+dominates, the caller's stream per batch, and the structural update.  The line also carries the
 whole-matrix weight pass, the STL-shaped layer (a short run of the same schedule on the first
 images of that workload, with its weight pass), the forward-pass throughput by batch size, and
 the CPU oracle on a bounded sample of the MNIST-shaped schedule on this host's cores (all
@@ -45,7 +49,7 @@ PEAK_BF16_MFMA_TFS = 2500.0
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
 # In the profiling pass after the timed region, every PROFILE_PERIOD-th launch of each kernel
-# is bracketed by events.
+# is timed.
 PROFILE_PERIOD = 1
 PROFILE_SYNC = 64             # steps of the profiling pass between two reads of the timers
 # Launches of the whole-matrix weight pass timed after the training run.
@@ -66,10 +70,14 @@ STL_WARMUP, STL_STEPS = 2, 16
 # (kernel_digest); a changed source reports null until measured again.  The sweep's figure
 # is for the counter run's average launch (MNIST shape: 7.65 batches per launch; STL shape:
 # 5.56), the weight pass's for every launch.
-_SWEEP_DIGEST = "278571dc66809b999bf3ff6e2317011da93ef5a377412c36dbfb8c74e2048839"
-_WEIGHT_DIGEST = "87a3330bbe43b98fcac5eb4c5ca2b78de1b1c0de15773fb4fcd66e8656d33ae4"
-MEASURED_TRAFFIC = {("mnist", _SWEEP_DIGEST): 92.81e6, ("stl", _SWEEP_DIGEST): 9863.75e6}
-MEASURED_WEIGHT_TRAFFIC = {("mnist", _WEIGHT_DIGEST): 21.77e6, ("stl", _WEIGHT_DIGEST): 2404.24e6}
+_SWEEP_DIGEST = "09b18091e61eed64d84faad69563bb73b5ee4fdc99dcee19b7fe35fa7b268136"
+_WEIGHT_DIGEST = "329f407e0161ecbbac0607fb9d21c5a0a53d6248efd521244ed72615f3c0d97b"
+MEASURED_TRAFFIC = {("mnist", _SWEEP_DIGEST): 92.61e6, ("stl", _SWEEP_DIGEST): 9813.76e6}
+MEASURED_WEIGHT_TRAFFIC = {("mnist", _WEIGHT_DIGEST): 21.76e6, ("stl", _WEIGHT_DIGEST): 2404.16e6}
+# The support kernel's, per training launch (the same counters and formulas; the launches of
+# the timing pass, which stamp their own duration, read the same).
+_SUPPORT_DIGEST = "c8dcdc430cafc6230ea9f8fbd0acd4e435d1500db73bd5e3a89819fd5bb6df6e"
+MEASURED_SUPPORT_TRAFFIC = {("mnist", _SUPPORT_DIGEST): 11.51e6, ("stl", _SUPPORT_DIGEST): 2689.77e6}
 
 
 def kernel_digest(csrc, files):
@@ -84,6 +92,7 @@ def kernel_digest(csrc, files):
 
 SWEEP_SOURCES = ("k_trace.hip", "bcpnn_internal.h", "device_common.h")
 WEIGHT_SOURCES = ("k_weights.hip", "bcpnn_internal.h", "device_common.h")
+SUPPORT_SOURCES = ("k_support.hip", "bcpnn_internal.h", "device_common.h")
 
 
 def sweep_sizes(sched, first, last):
@@ -200,7 +209,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic", "config": res["config"], "roofline": res["roofline"],
-        "mfma": res["mfma"], "contraction": res["contraction"],
+        "sweep": res["sweep"], "mfma": res["mfma"], "contraction": res["contraction"],
         "critical_path": res["critical_path"], "structural_update": res["structural_update"],
         "weight_pass": res["weight_pass"],
     }
@@ -210,7 +219,8 @@ def main():
                              profile_steps=STL_STEPS, launch=args.launch, profile_period=1)
         out["stl"] = {"value": r["value"], "unit": "samples/s", "ms_per_step": r["ms_per_step"],
                       "steps": STL_STEPS, "warmup": STL_WARMUP, "config": r["config"],
-                      "roofline": r["roofline"], "critical_path": r["critical_path"],
+                      "roofline": r["roofline"], "sweep": r["sweep"], "mfma": r["mfma"],
+                      "critical_path": r["critical_path"],
                       "structural_update": r["structural_update"],
                       "weight_pass": r["weight_pass"]}
         stage("inference sweep")
@@ -225,8 +235,9 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
                      launch="eager", profile_period=PROFILE_PERIOD):
     """Trains the workload's layer on its schedule: `warmup` untimed steps, `steps` timed
     between two synchronisations (ending with bcpnn_flush), then an untimed profiling pass of
-    the following steps with every kernel launch timed by events, structural updates and weight
-    passes timed the same way.  Returns the fields of the JSON line."""
+    the following steps with every kernel launch timed (events around the sweep, device-clock
+    stamps in the support and active-block kernels), structural updates and weight passes
+    timed by events.  Returns the fields of the JSON line."""
     import torch
     from paper_2106_05373_amd import bcpnn, synth
 
@@ -314,7 +325,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     last += n_other
 
     # ---- untimed profiling pass: the following steps, every profile_period-th launch of each
-    # kernel bracketed by events (sampled, so that the stream keeps the schedule's pace) -----
+    # kernel timed (sampled, so that the stream keeps the schedule's pace) ------------------
     stage(f"{w.name}: profiling pass of {profile_steps} steps")
     for k in bcpnn.KERNELS:
         layer.profile_read_kernel(k)                             # discard older records
@@ -356,7 +367,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     active = k_act * L.in_mcu * L.n_out
     E = L.n_in * L.n_out
 
-    # ---- roofline of the dominant kernel: the silent-element sweep -------------------------
+    # ---- the silent-element sweep against the HBM roofline ---------------------------------
     # Per launch it must read every Pij and write those of silent blocks (4 + 4 bytes per silent
     # element, 4 per active one), and read the split operands of each batch it applies once
     # (bf16 hi and lo of x and t, 4 bytes per element per padded batch row; with complement
@@ -378,7 +389,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     avg_sweep_s = sweep_ms / 1e3 / sweep_n
     achieved_gbs = bytes_per_launch / avg_sweep_s / 1e9
     traffic = MEASURED_TRAFFIC.get((traffic_key, kernel_digest(csrc, SWEEP_SOURCES)))
-    roofline = {
+    sweep = {
         "bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS,
         "unit": "GB/s", "frac": round(achieved_gbs / PEAK_HBM_GBS, 4), "traffic": traffic,
         "kernel": ("trace_sweep_pair" if pairs else "trace_sweep") +
@@ -393,7 +404,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
         "timing": f"profiling pass of {profile_steps} steps after the timed region, every "
-                  f"{profile_period}th launch of each kernel bracketed by events",
+                  f"{profile_period}th launch bracketed by events on its stream",
     }
 
     # ---- the joint-trace contraction against the bf16 matrix cores it runs on --------------
@@ -401,7 +412,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     # executed: three split-bf16 products per multiply-add.
     flops_alg = 2.0 * n_x * L.n_out * avg_b * per_sweep
     contraction = {
-        "kernel": roofline["kernel"].split(" ")[0], "dtype": "bf16 (hi/lo split, 3 products)",
+        "kernel": sweep["kernel"].split(" ")[0], "dtype": "bf16 (hi/lo split, 3 products)",
         "algorithmic_tflops": round(flops_alg / avg_sweep_s / 1e12, 3),
         "executed_tflops": round(3 * flops_alg / avg_sweep_s / 1e12, 3),
         "peak": PEAK_BF16_MFMA_TFS, "unit": "TFLOP/s",
@@ -421,12 +432,44 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "algorithmic_flops_per_launch": sup_flops, "avg_us": round(avg_sup_s * 1e6, 3),
         "timed_launches": sup_n,
     }
+    avg_act_s = act_ms / 1e3 / max(act_n, 1)
     critical_path = {
         "stream": "caller's: support then active-block trace kernel, every batch",
         "support_us": round(avg_sup_s * 1e6, 3),
-        "active_us": round(act_ms / 1e3 / max(act_n, 1) * 1e6, 3),
+        "active_us": round(avg_act_s * 1e6, 3),
         "batch_us": round(wall_s * 1e6 / max(steps, 1), 3),
     }
+
+    # ---- roofline of the dominant kernel: the one with the most GPU time per batch -----------
+    per_batch_us = {"support": avg_sup_s * 1e6, "active": avg_act_s * 1e6,
+                    "sweep": avg_sweep_s * 1e6 / per_sweep}
+    dominant = max(per_batch_us, key=per_batch_us.get)
+    share = {"dominant": dominant,
+             "us_per_batch": {k: round(v, 3) for k, v in per_batch_us.items()}}
+    if dominant == "sweep":
+        roofline = dict(sweep, **share)
+    else:
+        if dominant == "support":
+            name, flops, avg_s, n, dtype, peak = (
+                mfma["kernel"], sup_flops, avg_sup_s, sup_n, "f64", PEAK_F64_MFMA_TFS)
+            traffic_s = MEASURED_SUPPORT_TRAFFIC.get(
+                (traffic_key, kernel_digest(csrc, SUPPORT_SOURCES)))
+        else:
+            # the active blocks' joint-trace contraction, one product per multiply-add
+            name = ("trace_active_pair_kernel" if pairs else "trace_active_kernel") + \
+                   " (active-block trace, weight and marginal update, split-bf16 MFMA)"
+            flops = 2.0 * avg_b * k_act * (1 if pairs else L.in_mcu) * L.n_out
+            avg_s, n, dtype, peak, traffic_s = (avg_act_s, act_n, "bf16", PEAK_BF16_MFMA_TFS,
+                                                None)
+        achieved = flops / avg_s / 1e12
+        roofline = {
+            "bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": traffic_s, "kernel": name,
+            "dtype": dtype, "avg_us": round(avg_s * 1e6, 3), "timed_launches": n,
+            "algorithmic_flops_per_launch": flops,
+            "timing": f"profiling pass of {profile_steps} steps after the timed region, every "
+                      f"{profile_period}th launch stamped by the kernel with the device clock "
+                      "(first workgroup start to last workgroup end)", **share}
     su_s = su_ms / 1e3 / max(su_n, 1)
     structural_update = {
         "kernels": "mi_kernel + swap_kernel", "avg_us": round(su_s * 1e6, 3),
@@ -469,7 +512,8 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "parallelism": "single GPU",
     }
     return {"value": round(samples / wall_s, 1), "ms_per_step": round(wall_s * 1e3 / steps, 5),
-            "config": config, "roofline": roofline, "contraction": contraction, "mfma": mfma,
+            "config": config, "roofline": roofline, "sweep": sweep, "contraction": contraction,
+            "mfma": mfma,
             "critical_path": critical_path, "structural_update": structural_update,
             "weight_pass": weight_pass, "mask": mask}
 

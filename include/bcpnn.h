@@ -213,10 +213,11 @@ bcpnn_status bcpnn_set_state(bcpnn_layer *layer, const bcpnn_state_view *host_in
 bcpnn_status bcpnn_get_mi(bcpnn_layer *layer, double *mi_host);
 
 /* Kernel timing for measurement: with period n > 0, every n-th launch of the silent-block sweep
- * of the joint traces (of the active-block trace kernel when the mask has no silent block),
- * counting from the call, is bracketed by a pair of HIP events recorded on its stream right
- * before and after it (their interval is the kernel's execution plus the events' short passage
- * through the stream); n = 0 turns it off.  Each timed launch costs the stream a few
+ * of the joint traces, counting from the call, is bracketed by a pair of HIP events recorded on
+ * its stream right before and after it (their interval is the kernel's execution plus the
+ * events' short passage through the stream); when the mask has no silent block, the
+ * active-block trace kernel's launches are timed instead, by their own clock stamps (see
+ * bcpnn_profile_read_kernel); n = 0 turns it off.  Each timed launch costs the stream a few
  * microseconds, so a period of 10 or more keeps a throughput measurement nearly
  * unperturbed.  bcpnn_profile_read waits for both
  * streams and returns the summed duration (ms) and count of the timed launches since the last
@@ -230,8 +231,13 @@ bcpnn_status bcpnn_profile_read(bcpnn_layer *layer, double *total_ms, int32_t *l
  * contraction operands) or the active-block trace kernel of train_batch, the weight pass of
  * recompute_weights (w over the whole matrix; the bias kernel after it is not included), or
  * the structural update (from the start of the mutual-information kernel to the end of the
- * swap kernel; the queued sweep it applies first is not included).  profile_enable's period
- * applies to each kernel's own launch count.  Reads and clears that kernel's record only.
+ * swap kernel; the queued sweep it applies first is not included).  The support and active
+ * kernels, short launches on the caller's stream, are not bracketed by events: a timed launch
+ * stamps the device clock (hipDeviceAttributeWallClockRate) when its first workgroup starts and
+ * when its last one ends, and its duration is that span: the kernel's execution on the compute
+ * units (a kernel trace also counts the dispatch's start and completion, 1-2 us).
+ * profile_enable's period applies to each kernel's own launch count.  Reads and clears that
+ * kernel's record only.
  * Errors: EINVAL for an unknown kernel or NULL outputs. */
 typedef enum {
     BCPNN_KERNEL_SWEEP = 0,

@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <utility>
@@ -105,9 +106,11 @@ struct bcpnn_layer {
     bool mi_valid = false;
     bool failed = false;
     void* scratch = nullptr;             // this device's static scratch (resolved at create)
-    int32_t profile_every = 0;           // 0: off; n: every n-th launch of a kernel carries events
-    struct KernelTimer {                 // event pairs around the timed launches of one kernel
-        std::vector<std::pair<hipEvent_t, hipEvent_t>> events;
+    int32_t profile_every = 0;           // 0: off; n: every n-th launch of a kernel is timed
+    int clock_khz = 0;                   // rate of the device clock the stamps read
+    struct KernelTimer {                 // the timed launches of one kernel
+        std::vector<std::pair<hipEvent_t, hipEvent_t>> events;   // event pairs around them
+        std::vector<unsigned long long*> stamps;  // or device chunks of stamp slots
         size_t used = 0;
         int64_t launches = 0;
     };
@@ -204,11 +207,13 @@ void free_layer(bcpnn_layer* L) {
     }
     if (L->sweep_ready) (void)hipEventDestroy(L->sweep_ready);
     if (L->side) (void)hipStreamDestroy(L->side);
-    for (auto& tm : L->timers)
+    for (auto& tm : L->timers) {
         for (auto& ev : tm.events) {
             (void)hipEventDestroy(ev.first);
             (void)hipEventDestroy(ev.second);
         }
+        for (unsigned long long* p : tm.stamps) (void)hipFree(p);
+    }
     delete L;
 }
 
@@ -231,6 +236,74 @@ hipError_t timer_events(bcpnn_layer* L, int k, hipEvent_t* start, hipEvent_t* st
     *start = tm.events[tm.used].first;
     *stop = tm.events[tm.used].second;
     ++tm.used;
+    return hipSuccess;
+}
+
+// The kernels of train_batch on the caller's stream (support, active blocks) are short next to
+// the passage of an event through a busy stream, so they time themselves: each timed launch
+// gets a slot of start and end words that its workgroups stamp with the device clock; its
+// duration is the first start to the last end.
+constexpr size_t kStampChunk = 256;      // slots per device allocation
+constexpr size_t kSlotWords = 2 * bcpnn::kStampLanes;
+
+bool stamped(int k) { return k == BCPNN_KERNEL_SUPPORT || k == BCPNN_KERNEL_ACTIVE; }
+
+// Host image of blank slots: the starts at the largest value (atomic min), the ends at 0
+// (atomic max).
+const unsigned long long* blank_stamps() {
+    static const std::vector<unsigned long long> v = [] {
+        std::vector<unsigned long long> b(kSlotWords * kStampChunk, 0ull);
+        for (size_t i = 0; i < kStampChunk; ++i)
+            for (int l = 0; l < bcpnn::kStampLanes; ++l) b[kSlotWords * i + l] = ~0ull;
+        return b;
+    }();
+    return v.data();
+}
+
+// Stamp slot for this launch of kernel k when profiling selects it, else null.  A slot is
+// blank when handed out: chunks are blanked when allocated and their used slots when read.
+hipError_t timer_stamp(bcpnn_layer* L, int k, unsigned long long** stamp) {
+    *stamp = nullptr;
+    bcpnn_layer::KernelTimer& tm = L->timers[k];
+    if (L->profile_every <= 0 || tm.launches++ % L->profile_every != 0) return hipSuccess;
+    const size_t chunk = tm.used / kStampChunk;
+    if (chunk == tm.stamps.size()) {
+        const size_t bytes = kSlotWords * kStampChunk * sizeof(unsigned long long);
+        unsigned long long* p = nullptr;
+        hipError_t e = hipMalloc(&p, bytes);
+        if (e == hipSuccess) e = hipMemcpy(p, blank_stamps(), bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            if (p) (void)hipFree(p);
+            return e;
+        }
+        tm.stamps.push_back(p);
+    }
+    *stamp = tm.stamps[chunk] + kSlotWords * (tm.used % kStampChunk);
+    ++tm.used;
+    return hipSuccess;
+}
+
+// Sum (ms) of the durations in the used stamp slots of a timer, which are blanked again.  The
+// launches must be complete.  A slot no workgroup stamped (an empty grid) counts as zero.
+hipError_t read_stamps(bcpnn_layer* L, bcpnn_layer::KernelTimer& tm, double* sum_ms) {
+    *sum_ms = 0.0;
+    std::vector<unsigned long long> h(kSlotWords * kStampChunk);
+    for (size_t c = 0; c * kStampChunk < tm.used; ++c) {
+        const size_t n = std::min(kStampChunk, tm.used - c * kStampChunk);
+        const size_t bytes = kSlotWords * n * sizeof(unsigned long long);
+        hipError_t e = hipMemcpy(h.data(), tm.stamps[c], bytes, hipMemcpyDeviceToHost);
+        if (e == hipSuccess) e = hipMemcpy(tm.stamps[c], blank_stamps(), bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return e;
+        for (size_t i = 0; i < n; ++i) {
+            const unsigned long long* s = h.data() + kSlotWords * i;
+            unsigned long long t0 = ~0ull, t1 = 0;
+            for (int l = 0; l < bcpnn::kStampLanes; ++l) {
+                t0 = std::min(t0, s[l]);
+                t1 = std::max(t1, s[bcpnn::kStampLanes + l]);
+            }
+            if (t1 > t0) *sum_ms += (double)(t1 - t0) / L->clock_khz;
+        }
+    }
     return hipSuccess;
 }
 
@@ -436,6 +509,9 @@ bcpnn_status bcpnn_layer_create(const bcpnn_config* cfg, const uint8_t* mask_hos
     if (e == hipSuccess) e = hipGetDevice(&dev);
     if (e == hipSuccess)
         e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&L->clock_khz, hipDeviceAttributeWallClockRate, dev);
+    if (e == hipSuccess && L->clock_khz <= 0) e = hipErrorInvalidValue;
     const int64_t blocks = ((g.n_in + 31) / 32) * ((g.n_out + 31) / 32);
     if (e == hipSuccess) L->sweep_wgs = blocks <= kSmallSweepBlocksPerCu * (int64_t)n_cu ? n_cu : -1;
     // this device's static scratch, resolved here (the device is current) for the
@@ -520,11 +596,12 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     // the operand set is free once the sweep that read it last has run
     if (L->set_sweep[set] >= 0) HIP_TRY(L, wait_sweep(L, L->set_sweep[set]));
     L->set_sweep[set] = -1;
-    hipEvent_t s0, s1;
-    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_SUPPORT, &s0, &s1));
+    unsigned long long* s_stamp = nullptr;
+    HIP_TRY(L, timer_stamp(L, BCPNN_KERNEL_SUPPORT, &s_stamp));
     HIP_TRY(L, bcpnn::launch_support(L->stream, L->g, x_dev, B, L->w, L->b, L->act_list,
                                      L->act_count, L->max_active, L->cfg.gain, 0, y, nullptr,
-                                     nullptr, target_dev, &L->ops[set], s0, s1));
+                                     nullptr, target_dev, &L->ops[set], nullptr, nullptr,
+                                     s_stamp));
     const double a_eff = 1.0 - pow(1.0 - (double)L->cfg.alpha, (double)L->cfg.n_cycles);
     bcpnn::TraceArgs a;
     a.ops = L->ops[set];
@@ -544,6 +621,7 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
     a.eps = L->cfg.eps;
     a.bias_gain = L->cfg.bias_gain;
     a.drop_bits = L->drop_bits;
+    a.stamp = nullptr;
     if (!L->full_mask) {
         // The silent elements: swept once per kMaxSweepBatches batches on the side stream,
         // which needs only the operands (written above) and touches no element the active
@@ -551,10 +629,9 @@ bcpnn_status bcpnn_train_batch(bcpnn_layer* L, const float* x_dev, int32_t B,
         L->pend[L->n_pend++] = bcpnn_layer::Pending{set, B, a.c1, a.c2};
         if (L->n_pend == bcpnn::kMaxSweepBatches) HIP_TRY(L, launch_pending_sweep(L));
     }
-    hipEvent_t a0, a1;
-    HIP_TRY(L, timer_events(L, BCPNN_KERNEL_ACTIVE, &a0, &a1));
+    HIP_TRY(L, timer_stamp(L, BCPNN_KERNEL_ACTIVE, &a.stamp));
     HIP_TRY(L, bcpnn::launch_trace_active(L->stream, L->g, a, L->act_list, L->act_count,
-                                          L->max_active, a0, a1));
+                                          L->max_active, nullptr, nullptr));
     L->cur = 1 - L->cur;
     L->ops_cur = (set + 1) % kSets;
     return BCPNN_OK;
@@ -742,11 +819,14 @@ bcpnn_status bcpnn_profile_read_kernel(bcpnn_layer* L, int32_t kernel, double* t
     if (bcpnn_status st = input_check_result(L)) return st;
     bcpnn_layer::KernelTimer& tm = L->timers[kernel];
     double sum = 0.0;
-    for (size_t k = 0; k < tm.used; ++k) {
-        float ms = 0.0f;
-        HIP_TRY(L, hipEventElapsedTime(&ms, tm.events[k].first, tm.events[k].second));
-        sum += ms;
-    }
+    if (stamped(kernel))
+        HIP_TRY(L, read_stamps(L, tm, &sum));
+    else
+        for (size_t k = 0; k < tm.used; ++k) {
+            float ms = 0.0f;
+            HIP_TRY(L, hipEventElapsedTime(&ms, tm.events[k].first, tm.events[k].second));
+            sum += ms;
+        }
     *total_ms = sum;
     *launches = (int32_t)tm.used;
     tm.used = 0;

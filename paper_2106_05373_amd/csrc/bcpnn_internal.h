@@ -37,6 +37,35 @@ hipError_t launch_timed(void (*kernel)(Params...), dim3 grid, dim3 block, size_t
     return e;
 }
 
+// Launch-duration stamps (profiling of the short kernels of the caller's stream), on the
+// device's constant-rate clock (s_memrealtime): a launch's stamp holds kStampLanes start words
+// and as many end words; workgroup b takes the 64-bit atomic min of its start into start word
+// b % kStampLanes and the max of its end into end word b % kStampLanes (spread over many words,
+// so that the atomics of a large grid do not queue on one address).  The host initialises the
+// starts to the largest value and the ends to 0; the launch's span is the least start to the
+// greatest end.  A kernel stamps in a variant of its own (kOn): even a test of a null pointer
+// at both ends slows the short kernels measurably.  The end waits for the workgroup's memory
+// operations and all its waves; call it where every thread of the workgroup arrives.
+constexpr int kStampLanes = 64;
+template <bool kOn>
+__device__ __forceinline__ void stamp_start(unsigned long long* stamp) {
+    if constexpr (kOn) {
+        if (threadIdx.x == 0)
+            atomicMin(stamp + blockIdx.x % kStampLanes,
+                      (unsigned long long)__builtin_amdgcn_s_memrealtime());
+    }
+}
+template <bool kOn>
+__device__ __forceinline__ void stamp_end(unsigned long long* stamp) {
+    if constexpr (kOn) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0)
+            atomicMax(stamp + kStampLanes + blockIdx.x % kStampLanes,
+                      (unsigned long long)__builtin_amdgcn_s_memrealtime());
+    }
+}
+
 // Initial state: Pij = pij0, w = mask ? noise * (2u - 1) : 0 with u from SplitMix64.
 hipError_t launch_init_state(hipStream_t stream, const Geometry& g, const uint8_t* mask,
                              float pij0, float init_noise, uint64_t seed, int drop_bits,
@@ -103,7 +132,7 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
                           float* y, float* s, int32_t* winner, const float* target,
                           const TraceOperands* ops, hipEvent_t start = nullptr,
-                          hipEvent_t stop = nullptr);
+                          hipEvent_t stop = nullptr, unsigned long long* stamp = nullptr);
 
 // Largest number of active input units (active HCUs * in_mcu) of one hidden HCU that the
 // support kernel keeps in its LDS unit table.
@@ -130,6 +159,7 @@ struct TraceArgs {
     const uint8_t* mask;
     float eps, bias_gain;
     int drop_bits;
+    unsigned long long* stamp;   // launch-duration stamp (stamp_start / stamp_end), or null
 };
 // The elements of active blocks (the rows of each hidden HCU's active input units), their
 // weights, and Pi, Pj, b of every unit.  max_active as for launch_support.

@@ -24,6 +24,7 @@
 // MFMA f64 16x16x4 lane layout (verified on gfx950): A[i][k] from lane i + 16 k, B[k][j] from
 // lane j + 16 k, and lane l holds D[l / 16 + 4 r][l % 16] in result register r.
 #include <mutex>
+#include <type_traits>
 
 #include "bcpnn_internal.h"
 #include "device_common.h"
@@ -98,14 +99,19 @@ __device__ __forceinline__ void write_split_half(const float (&v)[kRows / 2], ui
 
 // kTilesPerWave: 16-column output tiles per wave, ceil(ceil(M_out / 16) / 8).
 // kVec: 4 when weight row segments can be read as float4 (M_out and N_out multiples of 4).
-template <int kTilesPerWave, int kVec, int kLeanSlots = 0>
+// kOps: training (the contraction operands are written); the forward pass is a variant of its
+// own, without that code (and, in a kernel trace, under a name of its own).  kStamp: the
+// launch stamps its start and end (training launches that profiling times).
+template <int kTilesPerWave, int kVec, int kLeanSlots, bool kOps, bool kStamp>
 __global__ void __launch_bounds__(kThreads)
 support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32_t B,
                const float* __restrict__ w, const float* __restrict__ bias,
                const int32_t* __restrict__ act_list, const int32_t* __restrict__ act_count,
                float gain, int mode, float* __restrict__ y, float* __restrict__ s,
                int32_t* __restrict__ winner, const float* __restrict__ target,
-               TraceOperands ops, int has_ops) {
+               TraceOperands ops, unsigned long long* stamp) {
+    constexpr bool has_ops = kOps;
+    stamp_start<kStamp>(stamp);
     // Highest wave priority: on a CU shared with the silent sweep (second stream), the SIMD
     // arbiter issues this kernel's instructions first.
     __builtin_amdgcn_s_setprio(3);
@@ -445,7 +451,10 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             }
         }
     }
-    if (!has_ops) return;
+    if (!has_ops) {
+        stamp_end<kStamp>(stamp);
+        return;
+    }
 
     // Contraction operands of this workgroup's share of the batch (rows row0 .. row0 + 15, one
     // k-step): the hidden HCU's columns of t (the activity above, or the target) and the input
@@ -495,6 +504,7 @@ support_kernel(Geometry g, SupportLayout lay, const float* __restrict__ x, int32
             split_store(p);
         }
     }
+    stamp_end<kStamp>(stamp);
 }
 
 constexpr size_t kLdsBudget = 120 * 1024;
@@ -543,13 +553,30 @@ size_t lds_bytes(const SupportLayout& L) {
     return table + (panels > tile ? panels : tile);
 }
 
+// Lets every support variant of one mode take dynamic LDS up to the workgroup's limit.
+template <bool kOps, bool kStamp>
+void raise_lds_limit() {
+    const void* all[] = {(const void*)support_kernel<1, 4, kLeanSlots, kOps, kStamp>,
+                         (const void*)support_kernel<1, 4, 0, kOps, kStamp>,
+                         (const void*)support_kernel<2, 4, 0, kOps, kStamp>,
+                         (const void*)support_kernel<4, 4, 0, kOps, kStamp>,
+                         (const void*)support_kernel<kMaxTilesPerWave, 4, 0, kOps, kStamp>,
+                         (const void*)support_kernel<1, 1, 0, kOps, kStamp>,
+                         (const void*)support_kernel<2, 1, 0, kOps, kStamp>,
+                         (const void*)support_kernel<4, 1, 0, kOps, kStamp>,
+                         (const void*)support_kernel<kMaxTilesPerWave, 1, 0, kOps, kStamp>};
+    for (const void* k : all)
+        (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+}
+
 }  // namespace
 
 hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x, int32_t B,
                           const float* w, const float* bias, const int32_t* act_list,
                           const int32_t* act_count, int32_t max_active, float gain, int mode,
                           float* y, float* s, int32_t* winner, const float* target,
-                          const TraceOperands* ops, hipEvent_t start, hipEvent_t stop) {
+                          const TraceOperands* ops, hipEvent_t start, hipEvent_t stop,
+                          unsigned long long* stamp) {
     const int vec = (g.out_mcu % 4 == 0 && g.n_out % 4 == 0) ? 4 : 1;
     SupportLayout lay = make_layout(g, B, max_active * g.in_mcu, vec);
     // A layer whose active rows take several chunks anyway stages fewer weight vectors per
@@ -563,40 +590,39 @@ hipError_t launch_support(hipStream_t stream, const Geometry& g, const float* x,
     const size_t lds = lds_bytes(lay);
     const int tpw = (lay.n_tiles + kWaves - 1) / kWaves;
     const int64_t blocks = (int64_t)lay.n_row_tiles * g.out_hcu;
-    // allow dynamic LDS beyond 64 KB (gfx950 has 160 KB per workgroup): raised once, for every
-    // variant, to the largest size a launch can ask for
+    // allow dynamic LDS beyond 64 KB (gfx950 has 160 KB per workgroup): raised once, for
+    // every variant a launch can pick, to the largest size a launch can ask for
     static std::once_flag raised;
     std::call_once(raised, [] {
-        const void* all[] = {(const void*)support_kernel<1, 4, kLeanSlots>,
-                             (const void*)support_kernel<1, 4>, (const void*)support_kernel<2, 4>,
-                             (const void*)support_kernel<4, 4>,
-                             (const void*)support_kernel<kMaxTilesPerWave, 4>,
-                             (const void*)support_kernel<1, 1>, (const void*)support_kernel<2, 1>,
-                             (const void*)support_kernel<4, 1>,
-                             (const void*)support_kernel<kMaxTilesPerWave, 1>};
-        for (const void* k : all)
-            (void)hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      (int)kLdsLimit);
+        raise_lds_limit<false, false>();
+        raise_lds_limit<true, false>();
+        raise_lds_limit<true, true>();
         (void)hipGetLastError();
     });
-    auto go = [&](auto kernel) {
-        const TraceOperands o = ops ? *ops : TraceOperands{};
-        // the events (when given) are recorded around the launch
-        return launch_timed(kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, start,
-                            stop, g, lay, x, B, w, bias, act_list, act_count, gain, mode, y,
-                            s, winner, target, o, ops ? 1 : 0);
+    auto pick = [&](auto ops_c, auto stamp_c) -> hipError_t {
+        constexpr bool O = decltype(ops_c)::value, S = decltype(stamp_c)::value;
+        auto go = [&](auto kernel) {
+            const TraceOperands o = ops ? *ops : TraceOperands{};
+            // the events (when given) are recorded around the launch
+            return launch_timed(kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream,
+                                start, stop, g, lay, x, B, w, bias, act_list, act_count, gain,
+                                mode, y, s, winner, target, o, stamp);
+        };
+        if (vec == 4) {
+            if (lean) return go(support_kernel<1, 4, kLeanSlots, O, S>);
+            if (tpw <= 1) return go(support_kernel<1, 4, 0, O, S>);
+            if (tpw <= 2) return go(support_kernel<2, 4, 0, O, S>);
+            if (tpw <= 4) return go(support_kernel<4, 4, 0, O, S>);
+            return go(support_kernel<kMaxTilesPerWave, 4, 0, O, S>);
+        }
+        if (tpw <= 1) return go(support_kernel<1, 1, 0, O, S>);
+        if (tpw <= 2) return go(support_kernel<2, 1, 0, O, S>);
+        if (tpw <= 4) return go(support_kernel<4, 1, 0, O, S>);
+        return go(support_kernel<kMaxTilesPerWave, 1, 0, O, S>);
     };
-    if (vec == 4) {
-        if (lean) return go(support_kernel<1, 4, kLeanSlots>);
-        if (tpw <= 1) return go(support_kernel<1, 4>);
-        if (tpw <= 2) return go(support_kernel<2, 4>);
-        if (tpw <= 4) return go(support_kernel<4, 4>);
-        return go(support_kernel<kMaxTilesPerWave, 4>);
-    }
-    if (tpw <= 1) return go(support_kernel<1, 1>);
-    if (tpw <= 2) return go(support_kernel<2, 1>);
-    if (tpw <= 4) return go(support_kernel<4, 1>);
-    return go(support_kernel<kMaxTilesPerWave, 1>);
+    if (!ops) return stamp ? hipErrorInvalidValue : pick(std::false_type{}, std::false_type{});
+    return stamp ? pick(std::true_type{}, std::true_type{})
+                 : pick(std::true_type{}, std::false_type{});
 }
 
 }  // namespace bcpnn

@@ -58,6 +58,8 @@
 // MFMA 32x32x16 bf16 lane layout (verified on gfx950): A[i][k] for k = 8 (l / 32) + 0..7 from
 // lane l = i + 32 (k / 8), B[k][j] likewise with j = l % 32, and lane l holds
 // D[8 (r / 4) + 4 (l / 32) + r % 4][l % 32] in result register r.
+#include <type_traits>
+
 #include "bcpnn_internal.h"
 #include "device_common.h"
 
@@ -518,17 +520,19 @@ trace_sweep_tile_kernel(Geometry g, SweepArgs a, int n_tj) {
 // Active blocks: one workgroup per (hidden HCU, 32 of its active input units, 4 column blocks
 // of the HCU), one wave per 32 x 32 block; workgroups past n_work store the marginal traces and
 // bias of every unit instead.
-template <int kDropBits>
+template <int kDropBits, bool kStamp>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_list,
                     const int32_t* __restrict__ act_count, int n_rt, int n_cgr, int n_work) {
     // Highest wave priority, as in the support kernel: it shares CUs with the silent sweep.
     __builtin_amdgcn_s_setprio(3);
+    stamp_start<kStamp>(a.stamp);
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
     const int nk = (a.B + 15) / 16;
     const int n_ks = a.ops.n_ks;
     if ((int)blockIdx.x >= n_work) {
         store_marginal(g, a, (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x, nk);
+        stamp_end<kStamp>(a.stamp);
         return;
     }
     // The x fragment pieces of the block rows (32 gathered units), the same for the four waves,
@@ -644,27 +648,29 @@ trace_active_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_lis
         load_x();
         contract(k0);
     }
-    if (!col_live) return;
-    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
+    if (col_live) {                                    // wave-uniform
+        const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
 
-    // ---- marginal traces of the block's rows and columns, and their logs --------------------
-    const float lp = fast_log(fmaxf(marginal_value(m, sums, st, u, nk, a), a.eps));
-    const float lpj = __shfl(lp, 32 + jl, 64);
+        // ---- marginal traces of the block's rows and columns, and their logs --------------------
+        const float lp = fast_log(fmaxf(marginal_value(m, sums, st, u, nk, a), a.eps));
+        const float lpj = __shfl(lp, 32 + jl, 64);
 
-    // ---- epilogue: joint trace and weight of every element of the block ----------------------
-    const bool jok = jl < cols;
+        // ---- epilogue: joint trace and weight of every element of the block ---------------------
+        const bool jok = jl < cols;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int il = il0 + 8 * (r >> 2) + (r & 3);
-        const float lpi = half_broadcast(lp, 8 * (r >> 2) + (r & 3), lane);
-        const float pn = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pold[r]));
-        const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
-        if (jok && il < rows) {
-            const int64_t e = (int64_t)ur[r] * n_out + jb;
-            a.pij[e] = pn;
-            a.w[e] = wv;
+        for (int r = 0; r < 16; ++r) {
+            const int il = il0 + 8 * (r >> 2) + (r & 3);
+            const float lpi = half_broadcast(lp, 8 * (r >> 2) + (r & 3), lane);
+            const float pn = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pold[r]));
+            const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
+            if (jok && il < rows) {
+                const int64_t e = (int64_t)ur[r] * n_out + jb;
+                a.pij[e] = pn;
+                a.w[e] = wv;
+            }
         }
     }
+    stamp_end<kStamp>(a.stamp);
 }
 
 
@@ -1275,17 +1281,19 @@ trace_sweep_pair_tile_sum_kernel(Geometry g, SweepArgs a, int n_tj) {
 // waves, one storing the first rows of the pairs and one the second, so that every wave keeps
 // the per-element work of the unpaired kernel.  Otherwise a workgroup covers four column blocks
 // and each wave stores both rows.
-template <int kDropBits, bool kSplit>
+template <int kDropBits, bool kSplit, bool kStamp>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 trace_active_pair_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ act_list,
                          const int32_t* __restrict__ act_count, int n_rt, int n_cgr,
                          int n_work) {
     __builtin_amdgcn_s_setprio(3);
+    stamp_start<kStamp>(a.stamp);
     const int n_in = (int)g.n_in, n_out = (int)g.n_out;
     const int nk = (a.B + 15) / 16;
     const int n_ks = a.ops.n_ks;
     if ((int)blockIdx.x >= n_work) {
         store_marginal(g, a, (int64_t)(blockIdx.x - n_work) * blockDim.x + threadIdx.x, nk);
+        stamp_end<kStamp>(a.stamp);
         return;
     }
     constexpr int kBlocks = kSplit ? kWaves / 2 : kWaves;     // column blocks per workgroup
@@ -1400,55 +1408,57 @@ trace_active_pair_kernel(Geometry g, TraceArgs a, const int32_t* __restrict__ ac
         load_x();
         contract(k0);
     }
-    if (!col_live) return;
-    const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
-    const bool jok = jl < cols;
+    if (col_live) {                                    // wave-uniform
+        const int rows = k_total - rt * 32 < 32 ? k_total - rt * 32 : 32;   // may be <= 0
+        const bool jok = jl < cols;
 
-    if constexpr (kSplit) {
-        const float* sums = row_lane ? a.ops.x_sum : a.ops.t_sum;
-        const int64_t st_m = row_lane ? n_in : n_out;
-        const int um = row_lane ? urow : jb;
-        const float cs = marginal_colsum(mr, sums, st_m, um, nk);
-        const float lp = fast_log(fmaxf(marginal_from_colsum(mr, cs, a), a.eps));
-        const float lpj = __shfl(lp, 32 + jl, 64);
-        const float st = __shfl(cs, 32 + jl, 64);          // column total of t
+        if constexpr (kSplit) {
+            const float* sums = row_lane ? a.ops.x_sum : a.ops.t_sum;
+            const int64_t st_m = row_lane ? n_in : n_out;
+            const int um = row_lane ? urow : jb;
+            const float cs = marginal_colsum(mr, sums, st_m, um, nk);
+            const float lp = fast_log(fmaxf(marginal_from_colsum(mr, cs, a), a.eps));
+            const float lpj = __shfl(lp, 32 + jl, 64);
+            const float st = __shfl(cs, 32 + jl, 64);          // column total of t
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int src = 8 * (r >> 2) + (r & 3);
-            const int il = il0 + src;
-            const float lpi = half_broadcast(lp, src, lane);
-            const float tv = par ? st - acc[r] : acc[r];
-            const float pn = to_storage<kDropBits>(fmaf(a.c2, tv, a.c1 * pe[r]));
-            const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
-            if (jok && il < rows) {
-                const int64_t e = (int64_t)(2 * pr[r] + par) * n_out + jb;
-                a.pij[e] = pn;
-                a.w[e] = wv;
+            for (int r = 0; r < 16; ++r) {
+                const int src = 8 * (r >> 2) + (r & 3);
+                const int il = il0 + src;
+                const float lpi = half_broadcast(lp, src, lane);
+                const float tv = par ? st - acc[r] : acc[r];
+                const float pn = to_storage<kDropBits>(fmaf(a.c2, tv, a.c1 * pe[r]));
+                const float wv = to_storage<kDropBits>(fast_log(fmaxf(pn, a.eps)) - lpi - lpj);
+                if (jok && il < rows) {
+                    const int64_t e = (int64_t)(2 * pr[r] + par) * n_out + jb;
+                    a.pij[e] = pn;
+                    a.w[e] = wv;
+                }
             }
-        }
-    } else {
-        const float lp = fast_log(fmaxf(marginal_value(mr, a.ops.x_sum, n_in, urow, nk, a), a.eps));
-        const float st = marginal_colsum(mc, a.ops.t_sum, n_out, jb, nk);
-        const float lpj = fast_log(fmaxf(marginal_from_colsum(mc, st, a), a.eps));
+        } else {
+            const float lp = fast_log(fmaxf(marginal_value(mr, a.ops.x_sum, n_in, urow, nk, a), a.eps));
+            const float st = marginal_colsum(mc, a.ops.t_sum, n_out, jb, nk);
+            const float lpj = fast_log(fmaxf(marginal_from_colsum(mc, st, a), a.eps));
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int src = 8 * (r >> 2) + (r & 3);
-            const int il = il0 + src;
-            const float lpe = half_broadcast(lp, src, lane);        // first unit of HCU il
-            const float lpo = half_broadcast(lp, 32 + src, lane);   // second unit
-            const float ne = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pe[r]));
-            const float no = to_storage<kDropBits>(fmaf(a.c2, st - acc[r], a.c1 * po[r]));
-            const float we = to_storage<kDropBits>(fast_log(fmaxf(ne, a.eps)) - lpe - lpj);
-            const float wo = to_storage<kDropBits>(fast_log(fmaxf(no, a.eps)) - lpo - lpj);
-            if (jok && il < rows) {
-                const int64_t e = (int64_t)(2 * pr[r]) * n_out + jb;
-                a.pij[e] = ne;
-                a.w[e] = we;
-                a.pij[e + n_out] = no;
-                a.w[e + n_out] = wo;
+            for (int r = 0; r < 16; ++r) {
+                const int src = 8 * (r >> 2) + (r & 3);
+                const int il = il0 + src;
+                const float lpe = half_broadcast(lp, src, lane);        // first unit of HCU il
+                const float lpo = half_broadcast(lp, 32 + src, lane);   // second unit
+                const float ne = to_storage<kDropBits>(fmaf(a.c2, acc[r], a.c1 * pe[r]));
+                const float no = to_storage<kDropBits>(fmaf(a.c2, st - acc[r], a.c1 * po[r]));
+                const float we = to_storage<kDropBits>(fast_log(fmaxf(ne, a.eps)) - lpe - lpj);
+                const float wo = to_storage<kDropBits>(fast_log(fmaxf(no, a.eps)) - lpo - lpj);
+                if (jok && il < rows) {
+                    const int64_t e = (int64_t)(2 * pr[r]) * n_out + jb;
+                    a.pij[e] = ne;
+                    a.w[e] = we;
+                    a.pij[e + n_out] = no;
+                    a.w[e + n_out] = wo;
+                }
             }
         }
     }
+    stamp_end<kStamp>(a.stamp);
 }
 
 }  // namespace
@@ -1546,19 +1556,25 @@ hipError_t launch_trace_active(hipStream_t stream, const Geometry& g, const Trac
     const int64_t n_cgr = active_col_groups(g, paired);
     const int64_t n_work = (int64_t)g.out_hcu * n_rt * n_cgr;
     const int64_t blocks = trace_active_workgroups(g, max_active, paired);
-    void (*kernel)(Geometry, TraceArgs, const int32_t*, const int32_t*, int, int, int) = nullptr;
-    switch (a.drop_bits * 4 + paired) {
-        case 0: kernel = trace_active_kernel<0>; break;
-        case 52: kernel = trace_active_kernel<13>; break;
-        case 64: kernel = trace_active_kernel<16>; break;
-        case 1: kernel = trace_active_pair_kernel<0, false>; break;
-        case 53: kernel = trace_active_pair_kernel<13, false>; break;
-        case 65: kernel = trace_active_pair_kernel<16, false>; break;
-        case 2: kernel = trace_active_pair_kernel<0, true>; break;
-        case 54: kernel = trace_active_pair_kernel<13, true>; break;
-        case 66: kernel = trace_active_pair_kernel<16, true>; break;
-        default: return hipErrorInvalidValue;
-    }
+    using Kernel = void (*)(Geometry, TraceArgs, const int32_t*, const int32_t*, int, int, int);
+    // the stamping variant when the launch carries a duration stamp
+    auto pick = [&](auto stamp_c) -> Kernel {
+        constexpr bool S = decltype(stamp_c)::value;
+        switch (a.drop_bits * 4 + paired) {
+            case 0: return trace_active_kernel<0, S>;
+            case 52: return trace_active_kernel<13, S>;
+            case 64: return trace_active_kernel<16, S>;
+            case 1: return trace_active_pair_kernel<0, false, S>;
+            case 53: return trace_active_pair_kernel<13, false, S>;
+            case 65: return trace_active_pair_kernel<16, false, S>;
+            case 2: return trace_active_pair_kernel<0, true, S>;
+            case 54: return trace_active_pair_kernel<13, true, S>;
+            case 66: return trace_active_pair_kernel<16, true, S>;
+            default: return nullptr;
+        }
+    };
+    const Kernel kernel = a.stamp ? pick(std::true_type{}) : pick(std::false_type{});
+    if (!kernel) return hipErrorInvalidValue;
     return launch_timed(kernel, dim3((unsigned)blocks), dim3(kWaves * 64), 0, stream, start,
                         stop, g, a, act_list, act_count, (int)n_rt, (int)n_cgr, (int)n_work);
 }
