@@ -46,6 +46,7 @@ METRIC = "train samples/s, MNIST-shaped 30x100 BCPNN layer; % MFMA peak, HBM GB/
 PEAK_HBM_GBS = 8000.0
 PEAK_F64_MFMA_TFS = 78.6
 PEAK_BF16_MFMA_TFS = 2500.0
+PEAK_F32_MFMA_TFS = 157.3
 # Batches whose silent-element updates one sweep applies (the library's kMaxSweepBatches).
 SWEEP_BATCHES = 8
 # In the profiling pass after the timed region, every PROFILE_PERIOD-th launch of each kernel
@@ -220,6 +221,7 @@ def main():
         out["stl"] = {"value": r["value"], "unit": "samples/s", "ms_per_step": r["ms_per_step"],
                       "steps": STL_STEPS, "warmup": STL_WARMUP, "config": r["config"],
                       "roofline": r["roofline"], "sweep": r["sweep"], "mfma": r["mfma"],
+                      "contraction": r["contraction"],
                       "critical_path": r["critical_path"],
                       "structural_update": r["structural_update"],
                       "weight_pass": r["weight_pass"]}
@@ -417,6 +419,11 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "executed_tflops": round(3 * flops_alg / avg_sweep_s / 1e12, 3),
         "peak": PEAK_BF16_MFMA_TFS, "unit": "TFLOP/s",
         "frac_algorithmic": round(flops_alg / avg_sweep_s / 1e12 / PEAK_BF16_MFMA_TFS, 4),
+        "frac_executed": round(3 * flops_alg / avg_sweep_s / 1e12 / PEAK_BF16_MFMA_TFS, 4),
+        # the fp32-accurate contraction's rate against the fp32 matrix cores it would otherwise
+        # run on (157.3 TFLOP/s dense)
+        "algorithmic_over_fp32_mfma_peak": round(flops_alg / avg_sweep_s / 1e12 /
+                                                 PEAK_F32_MFMA_TFS, 4),
     }
 
     # ---- the support GEMM on the fp64 matrix cores, and the caller's stream per batch --------

@@ -360,9 +360,11 @@ def test_inputs_that_are_not_pairs_fail_loudly(pairs):
 
 
 def test_profile_records_each_kernel():
-    """Dispatch-stamped timing of each train_batch kernel: with period 1, nine batches give nine
-    support and nine active-block launches and one sweep (of the first eight; reading leaves the
-    ninth batch queued), the flush a second sweep; an unknown kernel is rejected."""
+    """Timing of each train_batch kernel: with period 1, nine batches give nine support and nine
+    active-block launches (which stamp their own span) and one sweep (of the first eight;
+    reading leaves the ninth batch queued); three more batches read three launches of the same
+    order once the slots are read; the flush a second sweep; period 2 every second launch; an
+    unknown kernel is rejected."""
     import torch
     xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:9]]
     lay = bcpnn().Layer(workload_config(MNIST), workload_mask(MNIST))
@@ -374,9 +376,24 @@ def test_profile_records_each_kernel():
     ms_ac, n_ac = lay.profile_read_kernel("active")
     assert (n_sw, n_su, n_ac) == (1, 9, 9)
     assert ms_sw > 0 and ms_su > 0 and ms_ac > 0
+    # the support and active-block launches time themselves (device-clock stamps): each a
+    # microsecond to a few milliseconds
+    assert 1e-3 < ms_su / 9 < 5.0 and 1e-3 < ms_ac / 9 < 5.0, (ms_su, ms_ac)
     assert lay.profile_read_kernel("support") == (0.0, 0)          # reading clears
+    # reading leaves the stamp slots blank again: a slot still holding an earlier start would
+    # read the whole interval since then
+    for x in xs[:3]:
+        lay.train_batch(x)
+    ms2, n2 = lay.profile_read_kernel("support")
+    assert n2 == 3 and 1e-3 < ms2 / 3 < 5.0, (ms2, n2)
+    assert lay.profile_read_kernel("active")[1] == 3
     lay.flush()
     assert lay.profile_read_kernel("sweep")[1] == 1                 # the ninth batch's sweep
+    lay.profile_enable(2)                                           # every second launch
+    for x in xs[:4]:
+        lay.train_batch(x)
+    assert lay.profile_read_kernel("support")[1] == 2
+    assert lay.profile_read_kernel("active")[1] == 2
     B = bcpnn()
     import ctypes
     ms, n = ctypes.c_double(), ctypes.c_int32()
