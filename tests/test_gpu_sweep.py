@@ -64,6 +64,55 @@ def test_sweep_grouping_is_bitwise_invisible(pairs):
         assert np.array_equal(states[0][key].view(np.uint8), states[1][key].view(np.uint8)), key
 
 
+@pytest.mark.parametrize("shape,pairs,storage", [("mnist", 1, "f32"), ("mnist", 0, "bf16"),
+                                                  ("large", 1, "f32"), ("large", 0, "f32")])
+def test_timed_launches_compute_the_same_bits(shape, pairs, storage):
+    """The launches that time themselves (the support and active-block kernels with their
+    clock stamps, which the profiling pass of the benchmark runs) compute what the untimed ones
+    do: the same batches, a structural update among them, with profiling off and with every
+    launch timed, give bitwise identical activities and states.  The large layer's support
+    takes several chunks of active rows (its lean variant)."""
+    import torch
+    from pairs import gpu_config
+    if shape == "mnist":
+        cfg = workload_config(MNIST, alpha=0.02, complement_pairs=pairs, storage=storage)
+        mask = workload_mask(MNIST)
+        xs = _inputs()[:12]
+    else:
+        in_hcu, out_hcu, out_mcu = 4100, 21, 100
+        cfg = gpu_config(in_hcu, 2, out_hcu, out_mcu, 64, alpha=0.05, complement_pairs=pairs,
+                         storage=storage)
+        mask = np.stack([synth.random_mask(in_hcu, 1, 104, 70 + c)[:, 0]
+                         for c in range(out_hcu)], 1)
+        rng = np.random.default_rng(5)
+        xs = [synth.encode_pixels(rng.random((B, in_hcu)).astype(np.float32))
+              for B in (64, 40, 64, 23, 64, 1, 64, 64, 50, 64, 17, 64)]
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in xs]
+    runs = []
+    for period in (0, 1):
+        layer = bcpnn().Layer(cfg, mask)
+        layer.profile_enable(period)
+        ys = []
+        for k, x in enumerate(xs):
+            if k == 7:
+                layer.structural_update(count=False)
+            y = torch.empty((x.shape[0], layer.n_out), dtype=torch.float32, device="cuda")
+            layer.train_batch(x, y=y)
+            ys.append(y)
+        state = layer.get_state()
+        if period:
+            assert layer.profile_read_kernel("support")[1] == len(xs)
+            assert layer.profile_read_kernel("active")[1] == len(xs)
+        layer.profile_enable(0)
+        layer.close()
+        runs.append(([y.cpu().numpy() for y in ys], state))
+    (y0, s0), (y1, s1) = runs
+    for k, (a, b) in enumerate(zip(y0, y1)):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), f"activities of batch {k}"
+    for key in s0:
+        assert np.array_equal(s0[key].view(np.uint8), s1[key].view(np.uint8)), key
+
+
 class Moved:
     """Sum over the steps of a run of the oracle's per-step contraction term |P_new - c1 P_old|
     of each trace (what the contraction error of each step is relative to)."""
