@@ -63,22 +63,21 @@ INFERENCE_BATCHES = [1, 8, 32, 128, 512, 2048, 8192]
 STL_WARMUP, STL_STEPS = 2, 16
 
 # Memory traffic per launch (bytes between the L2 caches and the memory side: HBM and the
-# Infinity Cache) of the sweep kernel and of the weight pass, from rocprofv3 counter runs:
-# 128 TCC_EA0_RDREQ_128B + 64 TCC_EA0_RDREQ_64B + 32 TCC_EA0_RDREQ_32B read, and
-# 64 TCC_EA0_WRREQ_64B + 32 (TCC_EA0_WRREQ - TCC_EA0_WRREQ_64B) written, per dispatch (a
-# plain 256 MiB device copy reads exactly 256 MiB and writes 256 MiB by these formulas, so no
-# scale factor applies).  Keyed by workload and the SHA-256 of the kernel's sources
-# (kernel_digest); a changed source reports null until measured again.  The sweep's figure
-# is for the counter run's average launch (MNIST shape: 7.65 batches per launch; STL shape:
-# 5.56), the weight pass's for every launch.
+# Infinity Cache) of the support, the sweep and the weight pass, from two rocprofv3 counter runs
+# of the same command, FETCH_SIZE and then WRITE_SIZE (KiB per dispatch), each scaled by what
+# it reads for a plain 256 MiB device copy (`bench.py --calibrate-copy`: FETCH_SIZE 131084.5
+# KiB, WRITE_SIZE 262144 KiB, so factors 1.99981 and 1).  The request counters (128 RDREQ_128B
+# + 64 RDREQ_64B + 32 RDREQ_32B read, 64 WRREQ_64B + 32 (WRREQ - WRREQ_64B) written, exact for
+# the copy with no factor) give the same within 1.2%.  Keyed by workload and the SHA-256 of the
+# kernel's sources (kernel_digest); a changed source reports null until measured again.  The
+# sweep's figure is for the counter run's average launch (MNIST shape: 7.65 batches per launch;
+# STL shape: 5.56), the others' for every launch (the support's for its training launches).
 _SWEEP_DIGEST = "09b18091e61eed64d84faad69563bb73b5ee4fdc99dcee19b7fe35fa7b268136"
 _WEIGHT_DIGEST = "329f407e0161ecbbac0607fb9d21c5a0a53d6248efd521244ed72615f3c0d97b"
-MEASURED_TRAFFIC = {("mnist", _SWEEP_DIGEST): 92.61e6, ("stl", _SWEEP_DIGEST): 9813.76e6}
-MEASURED_WEIGHT_TRAFFIC = {("mnist", _WEIGHT_DIGEST): 21.76e6, ("stl", _WEIGHT_DIGEST): 2404.16e6}
-# The support kernel's, per training launch (the same counters and formulas; the launches of
-# the timing pass, which stamp their own duration, read the same).
 _SUPPORT_DIGEST = "c8dcdc430cafc6230ea9f8fbd0acd4e435d1500db73bd5e3a89819fd5bb6df6e"
-MEASURED_SUPPORT_TRAFFIC = {("mnist", _SUPPORT_DIGEST): 11.51e6, ("stl", _SUPPORT_DIGEST): 2689.77e6}
+MEASURED_TRAFFIC = {("mnist", _SWEEP_DIGEST): 92.71e6, ("stl", _SWEEP_DIGEST): 9855.62e6}
+MEASURED_WEIGHT_TRAFFIC = {("mnist", _WEIGHT_DIGEST): 21.90e6, ("stl", _WEIGHT_DIGEST): 2406.11e6}
+MEASURED_SUPPORT_TRAFFIC = {("mnist", _SUPPORT_DIGEST): 11.65e6, ("stl", _SUPPORT_DIGEST): 2692.97e6}
 
 
 def kernel_digest(csrc, files):
