@@ -17,15 +17,16 @@ After the timed region, an untimed profiling pass continues the same schedule wi
 kernel launch timed: the sweep, the weight pass and the structural update by HIP events
 recorded on their stream right before and after them, the support and active-block kernels
 (short launches on the caller's stream) by the device clock, stamped when their first
-workgroup starts and their last one ends; the kernel durations of the JSON line come from it: the roofline position of the
-dominant kernel (the one with the most GPU time per batch: the support, the active-block
-trace kernel, or the sweep over the silent elements of Pij, per batch of its launch), the
-sweep against the HBM roofline and the support against the fp64 matrix cores whichever
-dominates, the caller's stream per batch, and the structural update.  The line also carries the
-whole-matrix weight pass, the STL-shaped layer (a short run of the same schedule on the first
-images of that workload, with its weight pass), the forward-pass throughput by batch size, and
-the CPU oracle on a bounded sample of the MNIST-shaped schedule on this host's cores (all
-threads, and one).
+workgroup starts and their last one ends.  The kernel durations of the JSON line come from it:
+the roofline position of the dominant kernel (the one with the most time per batch on the
+caller's stream, which carries the schedule: the support, the active-block trace kernel, or,
+where it runs on that stream, the sweep over the silent elements of Pij, per batch of its
+launch), the sweep against the HBM roofline and the support against the fp64 matrix cores
+(both reported, whichever dominates), the caller's stream per batch, and the structural update.  The line also
+carries the whole-matrix weight pass, the STL-shaped layer (a short run of the same schedule on
+the first images of that workload, with its weight pass), the forward-pass throughput by batch
+size, and the CPU oracle on a bounded sample of the MNIST-shaped schedule on this host's cores
+(all threads, and one).
 """
 from __future__ import annotations
 
@@ -446,12 +447,17 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "batch_us": round(wall_s * 1e6 / max(steps, 1), 3),
     }
 
-    # ---- roofline of the dominant kernel: the one with the most GPU time per batch -----------
+    # ---- roofline of the dominant kernel: the one with the most time per batch on the caller's
+    # stream, which carries the schedule (a small layer's sweep runs on the layer's second
+    # stream beside the following batches, off that stream; a large layer's on it) -----------
     per_batch_us = {"support": avg_sup_s * 1e6, "active": avg_act_s * 1e6,
                     "sweep": avg_sweep_s * 1e6 / per_sweep}
-    dominant = max(per_batch_us, key=per_batch_us.get)
+    on_stream = [k for k in per_batch_us if k != "sweep" or not small_sweep]
+    dominant = max(on_stream, key=per_batch_us.get)
     share = {"dominant": dominant,
-             "us_per_batch": {k: round(v, 3) for k, v in per_batch_us.items()}}
+             "us_per_batch": {k: round(v, 3) for k, v in per_batch_us.items()},
+             "sweep_stream": "the layer's second stream, beside the following batches"
+                             if small_sweep else "the caller's"}
     if dominant == "sweep":
         roofline = dict(sweep, **share)
     else:
