@@ -64,6 +64,26 @@ def test_sweep_grouping_is_bitwise_invisible(pairs):
         assert np.array_equal(states[0][key].view(np.uint8), states[1][key].view(np.uint8)), key
 
 
+def test_profile_holds_more_launches_than_one_slot_chunk():
+    """More timed launches between two reads than one device allocation of stamp slots holds
+    (256): the library adds slots as it goes, and the read returns every launch, each of a
+    plausible duration, and leaves none behind."""
+    import torch
+    xs = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in _inputs()[:4]]
+    lay = bcpnn().Layer(workload_config(MNIST), workload_mask(MNIST))
+    lay.profile_enable(1)
+    n = 300
+    for k in range(n):
+        lay.train_batch(xs[k % len(xs)])
+    for kernel in ("support", "active"):
+        ms, m = lay.profile_read_kernel(kernel)
+        assert m == n, (kernel, m)
+        assert 1e-3 < ms / n < 5.0, (kernel, ms)
+        assert lay.profile_read_kernel(kernel) == (0.0, 0)
+    lay.profile_enable(0)
+    lay.close()
+
+
 @pytest.mark.parametrize("shape,pairs,storage", [("mnist", 1, "f32"), ("mnist", 0, "bf16"),
                                                   ("large", 1, "f32"), ("large", 0, "f32")])
 def test_timed_launches_compute_the_same_bits(shape, pairs, storage):
