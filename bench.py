@@ -375,6 +375,7 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
     # (bf16 hi and lo of x and t, 4 bytes per element per padded batch row; with complement
     # pairs x covers the first unit of each input HCU only, and the column sums of t per
     # 16-row tile are read as well).
+    every = "every launch" if profile_period == 1 else f"one launch in {profile_period}"
     sizes = sweep_sizes(sched, last, n_steps)
     # the library's choice of sweep: one workgroup per CU when the matrix has at most 64
     # 32 x 32 blocks per CU, LDS-staged tiles otherwise
@@ -405,8 +406,8 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
         "avg_us": round(avg_sweep_s * 1e6, 3), "timed_launches": sweep_n,
         "batches_per_launch": round(per_sweep, 3),
         "algorithmic_bytes_per_launch": bytes_per_launch,
-        "timing": f"profiling pass of {profile_steps} steps after the timed region, every "
-                  f"{profile_period}th launch bracketed by events on its stream",
+        "timing": f"profiling pass of {profile_steps} steps after the timed region, "
+                  f"{every} bracketed by events on its stream",
     }
 
     # ---- the joint-trace contraction against the bf16 matrix cores it runs on --------------
@@ -479,8 +480,8 @@ def measure_training(w, warmup, steps, pairs, profile_steps=None, n_images=None,
             "frac": round(achieved / peak, 4), "traffic": traffic_s, "kernel": name,
             "dtype": dtype, "avg_us": round(avg_s * 1e6, 3), "timed_launches": n,
             "algorithmic_flops_per_launch": flops,
-            "timing": f"profiling pass of {profile_steps} steps after the timed region, every "
-                      f"{profile_period}th launch stamped by the kernel with the device clock "
+            "timing": f"profiling pass of {profile_steps} steps after the timed region, "
+                      f"{every} stamped by the kernel with the device clock "
                       "(first workgroup start to last workgroup end)", **share}
     su_s = su_ms / 1e3 / max(su_n, 1)
     structural_update = {
